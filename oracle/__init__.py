@@ -1,0 +1,309 @@
+"""CPU oracle for the differential-oracle hot path -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow C implementation (ref_oracle.c, built with gcc, fp64, no
+fast-math, contraction off) of what the GPU library computes: the guarded
+seeded fill, the element-wise comparison of a candidate state against the
+reference state (paper section 3.2, Eq. 1 and iota; section 3.4 Tier-1/Tier-2
+checks), and the canary-guard check.  It shares no code with the GPU library
+and neither imports the other.  Only tests/, the smoke entry point and the
+bench's cpu_baseline leg may use it; the product path never does.
+
+This binding only marshals arguments (ctypes); every computation happens in
+ref_oracle.c.  ctypes releases the GIL during each call, so callers may run
+independent calls from a thread pool.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ref_oracle.c")
+_SO = os.path.join(_HERE, "libref_oracle.so")
+
+# codes of ref_oracle.h
+DTYPE = {"f32": 1, "bf16": 2, "f16": 3, "fp8e4m3": 4, "i32": 5, "i64": 6, "u8": 7}
+ESIZE = {1: 4, 2: 2, 3: 2, 4: 1, 5: 4, 6: 8, 7: 1}
+MODE = {"bitwise": 0, "tolerance": 1}
+NAN_POLICY = {"equal": 0, "strict": 1}
+DIST = {"normal": 0, "uniform_int": 1, "bits": 2, "const": 3}
+KIND = {"flip_bit": 1, "step_within": 2, "set_beyond": 3, "set_nan": 4, "set_inf": 5,
+        "guard_write_lo": 6, "guard_write_hi": 7}
+RATE = 0x100
+SIDES = {"candidate": 0, "both": 1}
+
+
+def build() -> str:
+    """Compile the oracle with gcc (always recompiles)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
+           "-ffp-contract=off", "-fno-fast-math", "-o", _SO + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_SO + ".tmp", _SO)
+    return _SO
+
+
+class RefAlloc(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("alloc_id", ctypes.c_uint32),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("stride", ctypes.c_int64),
+                ("guard_lo", ctypes.c_int64), ("guard_hi", ctypes.c_int64),
+                ("dist", ctypes.c_int32), ("saturate", ctypes.c_int32),
+                ("p0", ctypes.c_double), ("p1", ctypes.c_double),
+                ("i0", ctypes.c_int64), ("i1", ctypes.c_int64)]
+
+
+class RefInj(ctypes.Structure):
+    _fields_ = [("alloc", ctypes.c_uint32), ("kind", ctypes.c_uint32),
+                ("sides", ctypes.c_uint32), ("arg", ctypes.c_uint32),
+                ("index", ctypes.c_int64), ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
+class RefSeg(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("nan_policy", ctypes.c_int32), ("pad_", ctypes.c_int32),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("stride_a", ctypes.c_int64), ("stride_b", ctypes.c_int64),
+                ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
+class RefSegResult(ctypes.Structure):
+    _fields_ = [("mismatches", ctypes.c_uint64), ("first_mismatch", ctypes.c_int64),
+                ("bitwise_mismatches", ctypes.c_uint64), ("first_bitwise", ctypes.c_int64),
+                ("nonfinite_mismatches", ctypes.c_uint64),
+                ("max_abs", ctypes.c_double), ("max_rel", ctypes.c_double)]
+
+    def as_dict(self) -> Dict:
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class RefGuardResult(ctypes.Structure):
+    _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
+                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
+
+    def as_dict(self) -> Dict:
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_lib_handle: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(_SO):
+            build()
+        L = ctypes.CDLL(_SO)
+        P = ctypes.POINTER
+        vp = ctypes.c_void_p
+        L.ref_philox4x32_10.argtypes = [vp, vp, vp]
+        L.ref_esize.argtypes = [ctypes.c_int32]
+        L.ref_decode.argtypes = [ctypes.c_int32, ctypes.c_uint64, P(ctypes.c_double)]
+        L.ref_encode_f32.argtypes = [ctypes.c_int32, ctypes.c_float, ctypes.c_int]
+        L.ref_encode_f32.restype = ctypes.c_uint64
+        L.ref_log_u.argtypes = [ctypes.c_uint32]
+        L.ref_log_u.restype = ctypes.c_double
+        L.ref_normal.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int]
+        L.ref_normal.restype = ctypes.c_double
+        L.ref_element.argtypes = [P(RefAlloc), ctypes.c_int32, P(RefInj), ctypes.c_int64,
+                                  ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64]
+        L.ref_element.restype = ctypes.c_uint64
+        L.ref_canary_byte.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_int64]
+        L.ref_canary_byte.restype = ctypes.c_uint8
+        L.ref_fill_range.argtypes = [P(RefAlloc), ctypes.c_int32, P(RefInj), ctypes.c_int64,
+                                     ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
+                                     ctypes.c_int64, vp]
+        L.ref_diff_segment.argtypes = [P(RefSeg), vp, vp, P(RefSegResult)]
+        L.ref_guard_check.argtypes = [ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_int64,
+                                      vp, ctypes.c_int64, P(RefGuardResult)]
+        L.ref_decode_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, vp, vp]
+        L.ref_encode_f32_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, ctypes.c_int, vp]
+        L.ref_log_u_n.argtypes = [vp, ctypes.c_int64, vp]
+        L.ref_sincos_turns_n.argtypes = [vp, ctypes.c_int64, vp, vp]
+        L.ref_normal_n.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int, vp]
+        L.ref_philox_n.argtypes = [vp, vp, ctypes.c_int64, vp]
+        _lib_handle = L
+    return _lib_handle
+
+
+def _ptr(a: np.ndarray) -> int:
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+# --------------------------------------------------------------------------
+# scalar / bulk primitives (pinned by tests/test_oracle_*.py)
+# --------------------------------------------------------------------------
+
+def philox(ctr: Sequence[int], key: Sequence[int]) -> List[int]:
+    c = np.array(ctr, dtype=np.uint32)
+    k = np.array(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().ref_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return [int(v) for v in out]
+
+
+def philox_n(ctr: np.ndarray, key: np.ndarray) -> np.ndarray:
+    ctr = np.ascontiguousarray(ctr, dtype=np.uint32).reshape(-1, 4)
+    key = np.ascontiguousarray(key, dtype=np.uint32).reshape(-1, 2)
+    out = np.zeros_like(ctr)
+    lib().ref_philox_n(_ptr(ctr), _ptr(key), ctr.shape[0], _ptr(out))
+    return out
+
+
+def decode_n(dtype: str, raw: np.ndarray):
+    raw = np.ascontiguousarray(raw, dtype=np.uint64)
+    cls = np.zeros(raw.shape, dtype=np.int32)
+    val = np.zeros(raw.shape, dtype=np.float64)
+    lib().ref_decode_n(DTYPE[dtype], _ptr(raw), raw.size, _ptr(cls), _ptr(val))
+    return cls, val
+
+
+def encode_f32_n(dtype: str, x: np.ndarray, saturate: bool = False) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.zeros(x.shape, dtype=np.uint64)
+    lib().ref_encode_f32_n(DTYPE[dtype], _ptr(x), x.size, int(saturate), _ptr(out))
+    return out
+
+
+def log_u_n(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.uint32)
+    out = np.zeros(x.shape, dtype=np.float64)
+    lib().ref_log_u_n(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def sincos_turns_n(x: np.ndarray):
+    x = np.ascontiguousarray(x, dtype=np.uint32)
+    c = np.zeros(x.shape, dtype=np.float64)
+    s = np.zeros(x.shape, dtype=np.float64)
+    lib().ref_sincos_turns_n(_ptr(x), x.size, _ptr(c), _ptr(s))
+    return c, s
+
+
+def normal_n(xa: np.ndarray, xb: np.ndarray, which: int) -> np.ndarray:
+    xa = np.ascontiguousarray(xa, dtype=np.uint32)
+    xb = np.ascontiguousarray(xb, dtype=np.uint32)
+    out = np.zeros(xa.shape, dtype=np.float64)
+    lib().ref_normal_n(_ptr(xa), _ptr(xb), xa.size, which, _ptr(out))
+    return out
+
+
+def canary_byte(seed: int, alloc_id: int, side: int, p: int) -> int:
+    return int(lib().ref_canary_byte(seed, alloc_id, side, p))
+
+
+# --------------------------------------------------------------------------
+# workload-level helpers (workloads.Workload -> oracle structs)
+# --------------------------------------------------------------------------
+
+def ref_allocs(w) -> ctypes.Array:
+    arr = (RefAlloc * max(1, len(w.allocs)))()
+    for k, a in enumerate(w.allocs):
+        arr[k] = RefAlloc(DTYPE[a.dtype], a.alloc_id, a.rows, a.cols, a.stride, a.guard_lo,
+                          a.guard_hi, DIST[a.dist], int(a.saturate), a.p0, a.p1, a.i0, a.i1)
+    return arr
+
+
+def ref_injections(w) -> ctypes.Array:
+    arr = (RefInj * max(1, len(w.injections)))()
+    for t, j in enumerate(w.injections):
+        kind = KIND[j.kind]
+        index = j.index
+        if j.rate is not None:
+            kind |= RATE
+            index = int(round(j.rate * 2.0 ** 32))
+        arg = j.arg & 0xFFFFFFFF
+        arr[t] = RefInj(j.alloc, kind, SIDES[j.sides], arg, index, j.atol, j.rtol)
+    return arr
+
+
+class Prepared:
+    """Oracle structs of one workload, built once."""
+
+    def __init__(self, w):
+        self.w = w
+        self.allocs = ref_allocs(w)
+        self.inj = ref_injections(w)
+        self.n_inj = len(w.injections)
+
+    def element(self, k: int, variant: int, i: int) -> int:
+        return int(lib().ref_element(self.allocs, k, self.inj, self.n_inj, self.w.seed, variant, i))
+
+    def fill_range(self, k: int, variant: int, off: int, nbytes: int) -> np.ndarray:
+        out = np.empty(nbytes, dtype=np.uint8)
+        rc = lib().ref_fill_range(self.allocs, k, self.inj, self.n_inj, self.w.seed, variant,
+                                  off, nbytes, _ptr(out) if nbytes else None)
+        if rc != 0:
+            raise ValueError("oracle fill rejected the range")
+        return out
+
+    def fill_alloc(self, k: int, variant: int, threads: int = 1) -> np.ndarray:
+        total = self.w.allocs[k].total_bytes
+        if threads <= 1 or total < (1 << 20):
+            return self.fill_range(k, variant, 0, total)
+        from concurrent.futures import ThreadPoolExecutor
+        step = -(-total // (threads * 4))
+        step = -(-step // 16) * 16
+        parts = [(o, min(step, total - o)) for o in range(0, total, step)]
+        with ThreadPoolExecutor(threads) as ex:
+            chunks = list(ex.map(lambda p: self.fill_range(k, variant, p[0], p[1]), parts))
+        return np.concatenate(chunks)
+
+    def fill_arena(self, variant: int, threads: int = 1) -> np.ndarray:
+        arena = np.zeros(self.w.arena_bytes, dtype=np.uint8)
+        for k, a in enumerate(self.w.allocs):
+            o = self.w.offsets[k]
+            arena[o:o + a.total_bytes] = self.fill_alloc(k, variant, threads)
+        return arena
+
+
+def diff_segment(dtype: str, mode: str, nan_policy: str, rows: int, cols: int,
+                 stride_a: int, stride_b: int, atol: float, rtol: float,
+                 a: np.ndarray, b: np.ndarray, a_off: int = 0, b_off: int = 0) -> Dict:
+    """a, b: uint8 arrays; a_off/b_off: byte offset of element (0,0)."""
+    seg = RefSeg(DTYPE[dtype], MODE[mode], NAN_POLICY[nan_policy], 0, rows, cols, stride_a,
+                 stride_b, atol, rtol)
+    res = RefSegResult()
+    a = np.ascontiguousarray(a).view(np.uint8)
+    b = np.ascontiguousarray(b).view(np.uint8)
+    rc = lib().ref_diff_segment(ctypes.byref(seg), _ptr(a) + a_off, _ptr(b) + b_off, ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle diff rejected the segment")
+    return res.as_dict()
+
+
+def diff_workload(w, cand: np.ndarray, ref: np.ndarray, threads: int = 1) -> List[Dict]:
+    """Compares every Compare entry of `w`; cand/ref are whole arenas (uint8)."""
+    def one(c):
+        a = w.allocs[c.alloc]
+        off = w.data_offset(c.alloc)
+        return diff_segment(a.dtype, c.mode, c.nan_policy, a.rows, a.cols, a.stride, a.stride,
+                            c.atol, c.rtol, cand, ref, off, off)
+    if threads <= 1:
+        return [one(c) for c in w.compares]
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(one, w.compares))
+
+
+def guard_check(seed: int, alloc_id: int, lo: np.ndarray, hi: np.ndarray) -> Dict:
+    lo = np.ascontiguousarray(lo, dtype=np.uint8)
+    hi = np.ascontiguousarray(hi, dtype=np.uint8)
+    res = RefGuardResult()
+    lib().ref_guard_check(seed, alloc_id, _ptr(lo) if lo.size else None, lo.size,
+                          _ptr(hi) if hi.size else None, hi.size, ctypes.byref(res))
+    return res.as_dict()
+
+
+def guard_workload(w, arena: np.ndarray) -> List[Dict]:
+    out = []
+    for k, a in enumerate(w.allocs):
+        o = w.offsets[k]
+        lo = arena[o:o + a.guard_lo]
+        h0 = o + a.guard_lo + a.data_bytes
+        hi = arena[h0:h0 + a.guard_hi]
+        out.append(guard_check(w.seed, a.alloc_id, lo, hi))
+    return out

@@ -1,0 +1,116 @@
+/*
+ * ref_oracle.h -- the CPU oracle's own interface (test infrastructure only).
+ *
+ * This header belongs to the plain, slow CPU reference that the GPU library is
+ * checked against.  It shares no code, header, table or constant with the GPU
+ * library: every struct and constant here is declared independently, from the
+ * definitions of the differential oracle (paper section 3.2, Eq. 1 and the
+ * predicate iota; section 3.4, "Tier 1" guarded synthesis and the Tier-2
+ * byte-exact checks).  Only tests/, the smoke entry point and the bench's
+ * cpu_baseline leg load it.
+ */
+#ifndef REF_ORACLE_H
+#define REF_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element types */
+enum { REF_F32 = 1, REF_BF16 = 2, REF_F16 = 3, REF_FP8E4M3 = 4, REF_I32 = 5, REF_I64 = 6, REF_U8 = 7 };
+/* comparison modes and NaN policies */
+enum { REF_BITWISE = 0, REF_TOLERANCE = 1 };
+enum { REF_NAN_EQUAL = 0, REF_NAN_STRICT = 1 };
+/* value distributions of a fill */
+enum { REF_NORMAL = 0, REF_UNIFORM_INT = 1, REF_BITS = 2, REF_CONST = 3 };
+/* injection kinds; REF_RATE is or-ed into the kind of a Bernoulli rule */
+enum {
+  REF_FLIP_BIT = 1, REF_STEP_WITHIN = 2, REF_SET_BEYOND = 3, REF_SET_NAN = 4, REF_SET_INF = 5,
+  REF_GUARD_WRITE_LO = 6, REF_GUARD_WRITE_HI = 7
+};
+#define REF_RATE 0x100u
+enum { REF_SIDE_CANDIDATE = 0, REF_SIDE_BOTH = 1 };
+
+typedef struct {
+  int32_t dtype;
+  uint32_t alloc_id;       /* logical buffer id, identical on both sides */
+  int64_t rows, cols, stride;   /* elements */
+  int64_t guard_lo, guard_hi;   /* bytes */
+  int32_t dist;
+  int32_t saturate;        /* fp8: clamp to +-448 before rounding */
+  double p0, p1;           /* NORMAL mean/std; CONST value */
+  int64_t i0, i1;          /* UNIFORM_INT [i0, i1); CONST integer value */
+} ref_alloc;
+
+typedef struct {
+  uint32_t alloc;          /* index into the allocation array */
+  uint32_t kind;           /* REF_* kind, optionally | REF_RATE */
+  uint32_t sides;          /* REF_SIDE_* */
+  uint32_t arg;            /* bit index (0xffffffff = random) / Inf sign / guard byte count */
+  int64_t index;           /* element index, guard byte offset, or (RATE) threshold T */
+  double atol, rtol;       /* tolerance targeted by SET_BEYOND */
+} ref_inj;
+
+typedef struct {
+  int32_t dtype, mode, nan_policy, pad_;
+  int64_t rows, cols, stride_a, stride_b;  /* elements */
+  double atol, rtol;
+} ref_seg;
+
+typedef struct {
+  uint64_t mismatches;
+  int64_t first_mismatch;
+  uint64_t bitwise_mismatches;
+  int64_t first_bitwise;
+  uint64_t nonfinite_mismatches;
+  double max_abs, max_rel;
+} ref_seg_result;
+
+typedef struct {
+  uint64_t bad_lo, bad_hi;
+  int64_t first_bad_lo, first_bad_hi;
+} ref_guard_result;
+
+/* Philox4x32-10 block function (Salmon et al., SC'11). */
+void ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* element codecs */
+int ref_esize(int32_t dtype);
+/* class: 0 finite, 1 +Inf, 2 -Inf, 3 NaN; *value = exact fp64 value when finite */
+int ref_decode(int32_t dtype, uint64_t raw, double* value);
+uint64_t ref_encode_f32(int32_t dtype, float x, int saturate);
+
+/* the fill's own transcendental pieces (exposed for pinning against libm) */
+double ref_log_u(uint32_t x);                       /* ln((x + 0.5) * 2^-32) */
+void ref_sincos_turns(uint32_t x, double* c, double* s);   /* cos/sin(2*pi*x*2^-32) */
+double ref_normal(uint32_t xa, uint32_t xb, int which);    /* Box-Muller: which 0 cos, 1 sin */
+
+/* raw bits of element i of allocation k as written by a fill of `variant` */
+uint64_t ref_element(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64_t n_inj,
+                     uint64_t seed, uint32_t variant, int64_t i);
+uint8_t ref_canary_byte(uint64_t seed, uint32_t alloc_id, int side, int64_t p);
+
+/* Writes bytes [off, off + nbytes) of allocation k (offsets from its first lo-guard byte). */
+int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64_t n_inj,
+                   uint64_t seed, uint32_t variant, int64_t off, int64_t nbytes, uint8_t* out);
+
+/* Compares one segment: a, b point at element (0,0) of candidate and reference. */
+int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res);
+
+/* Guard check of one allocation: lo/hi point at the first byte of each guard (may be NULL if 0). */
+int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t n_lo,
+                    const uint8_t* hi, int64_t n_hi, ref_guard_result* res);
+
+/* bulk loops over the scalar functions above (used by the pin tests) */
+void ref_decode_n(int32_t dtype, const uint64_t* raw, int64_t n, int32_t* cls, double* value);
+void ref_encode_f32_n(int32_t dtype, const float* x, int64_t n, int saturate, uint64_t* out);
+void ref_log_u_n(const uint32_t* x, int64_t n, double* out);
+void ref_sincos_turns_n(const uint32_t* x, int64_t n, double* c, double* s);
+void ref_normal_n(const uint32_t* xa, const uint32_t* xb, int64_t n, int which, double* out);
+void ref_philox_n(const uint32_t* ctr, const uint32_t* key, int64_t n, uint32_t* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
