@@ -1,0 +1,254 @@
+/*
+ * asmevo.h -- C ABI of the MI355X (gfx950) differential-oracle library.
+ *
+ * The differential oracle decides whether a candidate kernel K' is
+ * functionally equivalent to the original code object K0 on an input x
+ * (AsmEvo, section 3.2, Eq. 1): its output state K'(x) is compared against the
+ * reference state O(x) = run(K0, x) under the same launch.  Floating-point
+ * outputs are checked against a tolerance, integer buffers, opaque state and
+ * guard regions byte-exactly (section 3.4, Tier 2), and the predicate iota
+ * additionally requires intact out-of-bounds guards, which Tier-1 synthesis
+ * places around every allocation as canary-initialised regions (section 3.4,
+ * Tier 1).  This library provides the data-parallel part of that check:
+ *
+ *   asmevo_fill_guarded   seeded guarded states (canaries, values, pads,
+ *                         injected candidate differences)        (sec. 3.4)
+ *   asmevo_diff_segments  element-wise compare of many buffers in one launch,
+ *                         per-buffer counts / first index / max abs / max rel
+ *                                                          (sec. 3.2, Eq. 1)
+ *   asmevo_guard_check    canary integrity of every guard region  (sec. 3.2
+ *                         iota, sec. 3.4)
+ *
+ * Conventions for every call:
+ *  - All addresses inside descriptors and all result pointers are HIP device
+ *    addresses on the current device.  Descriptor arrays (`allocs`, `inj`,
+ *    `segs`) are host memory: they are read and copied during the call, so the
+ *    caller may free or reuse them on return.
+ *  - `workspace` is device memory of at least asmevo_workspace_bytes(...)
+ *    bytes, owned by the caller; the call stages its descriptor tables there.
+ *    It must not be reused by another call until this call's work on `stream`
+ *    has completed.  The library allocates no memory of its own.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *    asynchronously; results are defined once the stream has been
+ *    synchronised.  The descriptor upload is a host-to-device copy from
+ *    pageable memory, which HIP performs synchronously with the host.
+ *  - Return value: ASMEVO_OK (0) or a negative status.  Argument errors are
+ *    detected before anything is enqueued.  A failing HIP call returns
+ *    ASMEVO_E_HIP and asmevo_last_hip_error() gives the hipError_t code.
+ *  - Element indices are logical row-major: i = r * cols + c, independent of
+ *    row strides; -1 means "none".
+ *  - Results are exact (integer counts, minimum indices, maxima of correctly
+ *    rounded fp64 values), so they do not depend on launch geometry or
+ *    scheduling and repeat bit-for-bit (the paper repeats each check three
+ *    times, section 4.1).
+ */
+#ifndef ASMEVO_H
+#define ASMEVO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ASMEVO_ABI_VERSION 1
+
+typedef int32_t asmevo_status;
+enum {
+  ASMEVO_OK = 0,
+  ASMEVO_E_INVALID = -1,      /* malformed descriptor or argument */
+  ASMEVO_E_UNSUPPORTED = -2,  /* valid but not supported (e.g. +-Inf in fp8 e4m3) */
+  ASMEVO_E_WORKSPACE = -3,    /* workspace missing or smaller than required */
+  ASMEVO_E_HIP = -4           /* a HIP runtime call failed */
+};
+
+/* element types */
+enum {
+  ASMEVO_F32 = 1,        /* IEEE binary32 */
+  ASMEVO_BF16 = 2,       /* bfloat16: the top half of a binary32 */
+  ASMEVO_F16 = 3,        /* IEEE binary16 */
+  ASMEVO_FP8_E4M3 = 4,   /* OCP 8-bit E4M3 (fn): bias 7, no Inf, 0x7F/0xFF NaN, max 448 */
+  ASMEVO_I32 = 5,
+  ASMEVO_I64 = 6,
+  ASMEVO_U8 = 7          /* opaque bytes */
+};
+
+/* comparison mode of a segment */
+enum {
+  ASMEVO_BITWISE = 0,    /* raw bits must be equal (any dtype) */
+  ASMEVO_TOLERANCE = 1   /* float dtypes only: |a - b| <= atol + rtol * |b| */
+};
+
+/* NaN policy of a TOLERANCE segment */
+enum {
+  ASMEVO_NAN_EQUAL = 0,  /* NaN matches NaN (sign and payload ignored) */
+  ASMEVO_NAN_STRICT = 1  /* a NaN never matches, not even identical bits */
+};
+
+/* value distribution of an allocation's data elements */
+enum {
+  ASMEVO_DIST_NORMAL = 0,       /* N(p0, p1^2): Box-Muller, then fp32 (RNE), then dtype (RNE) */
+  ASMEVO_DIST_UNIFORM_INT = 1,  /* integers uniform in [i0, i1), 0 < i1 - i0 <= 2^32 */
+  ASMEVO_DIST_BITS = 2,         /* raw generator bytes */
+  ASMEVO_DIST_CONST = 3         /* p0 (float dtypes, via fp32) or i0 (integer dtypes) */
+};
+#define ASMEVO_FILL_SATURATE 1u  /* fp8: clamp to +-448 before rounding */
+
+/*
+ * One guarded allocation (section 3.4, Tier 1: allocations carry guard
+ * regions initialised with canaries).  Memory layout from `base`:
+ *   [guard_lo bytes][data: rows rows of `stride` elements, the last row
+ *   holding only `cols`][guard_hi bytes]
+ * i.e. data bytes = ((rows - 1) * stride + cols) * element size (0 if rows
+ * or cols is 0).  Requirements: base 16-byte aligned (fill) or non-null
+ * (guard check); rows, cols >= 0; stride >= cols; guard_lo a multiple of the
+ * element size; guard sizes >= 0.  `alloc_id` is the logical buffer id and
+ * must be the same for the candidate's and the reference's copy of a buffer:
+ * it keys the generator, so both copies get identical values, pads and
+ * canaries.
+ */
+typedef struct {
+  uint64_t base;
+  int64_t rows, cols, stride;   /* elements */
+  int64_t guard_lo, guard_hi;   /* bytes */
+  uint32_t dtype, alloc_id;
+  uint32_t dist, flags;         /* ASMEVO_DIST_*, ASMEVO_FILL_* */
+  double p0, p1;
+  int64_t i0, i1;
+} asmevo_alloc;
+
+/* kinds of injected differences; ASMEVO_INJ_RATE is or-ed into `kind` to make
+ * a Bernoulli rule over every element instead of one element */
+enum {
+  ASMEVO_INJ_FLIP_BIT = 1,       /* flip bit `arg` (0xFFFFFFFF: a random bit) */
+  ASMEVO_INJ_STEP_WITHIN = 2,    /* move the magnitude one unit in the last place (float dtypes) */
+  ASMEVO_INJ_SET_BEYOND = 3,     /* a = b - sign(b) * 4 * (atol + rtol*|b|) (float dtypes) */
+  ASMEVO_INJ_SET_NAN = 4,        /* canonical quiet NaN (float dtypes) */
+  ASMEVO_INJ_SET_INF = 5,        /* +Inf (arg 0) or -Inf (arg 1); not for fp8 e4m3 */
+  ASMEVO_INJ_GUARD_WRITE_LO = 6, /* invert `arg` canary bytes of the lo guard from byte `index` */
+  ASMEVO_INJ_GUARD_WRITE_HI = 7  /* same for the hi guard (an out-of-bounds write) */
+};
+#define ASMEVO_INJ_RATE 0x100u
+enum { ASMEVO_SIDE_CANDIDATE = 0, ASMEVO_SIDE_BOTH = 1 };
+
+/*
+ * One injected difference.  A fill with variant 0 (the reference) applies only
+ * entries with sides == ASMEVO_SIDE_BOTH; a fill with variant v > 0 applies
+ * every entry.  Element entries act on the element's base value; when several
+ * entries hit one element the last in the array wins, and element entries
+ * override Bernoulli rules.  For a RATE rule `index` holds the threshold T
+ * (0 <= T <= 2^32): element i is selected iff its SELECT draw is below T.
+ */
+typedef struct {
+  uint32_t alloc;      /* index into the allocation array of the call */
+  uint32_t kind;
+  uint32_t sides;
+  uint32_t arg;
+  int64_t index;       /* element index, guard byte offset, or RATE threshold */
+  double atol, rtol;   /* tolerance targeted by SET_BEYOND */
+} asmevo_injection;
+
+/*
+ * asmevo_fill_guarded -- writes every byte of each allocation: lo canary,
+ * data elements from the allocation's distribution, row-pad bytes, hi
+ * canary; then applies the injections that `variant` selects (section 3.4,
+ * Tier 1: deterministic seeded inputs with canary-initialised guards).
+ * Deterministic: a pure function of (descriptors, seed, variant).
+ * variant: 0 = reference state, 1..65535 = candidate state number.
+ * Allocations must not overlap.  Errors: ASMEVO_E_INVALID for malformed
+ * descriptors, overlapping allocations, NORMAL/BITS on integer dtypes mixed
+ * with fp-only injections, out-of-range indices; ASMEVO_E_UNSUPPORTED for
+ * SET_INF on fp8 e4m3 or more than 16 RATE rules on one allocation.
+ */
+asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
+                                  const asmevo_injection* inj, int64_t n_inj,
+                                  uint64_t seed, uint32_t variant,
+                                  void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * One compared buffer pair: `a` is the candidate state K'(x), `b` the
+ * reference O(x) (section 3.2: Delta = K'(x) - O(x); the relative term is
+ * scaled by the reference).  a and b address element (0,0); row r starts at
+ * a + r * stride_a elements (b likewise); strides >= cols; a and b aligned to
+ * the element size.  TOLERANCE requires a float dtype and finite
+ * atol, rtol >= 0.
+ */
+typedef struct {
+  uint64_t a, b;
+  uint32_t dtype, mode, nan_policy, reserved;
+  int64_t rows, cols, stride_a, stride_b;   /* elements */
+  double atol, rtol;
+} asmevo_segment;
+
+/*
+ * Per-segment result (56 bytes).  TOLERANCE mode, per element pair:
+ *   identical bits: match, unless b is NaN under NAN_STRICT;
+ *   a or b NaN: match iff both are NaN and the policy is NAN_EQUAL;
+ *   a or b infinite (bits differ): mismatch;
+ *   both finite: d = |A - B| and t = atol + rtol*|B| in fp64 with two
+ *     roundings (no fused multiply-add), match iff d <= t.
+ * `nonfinite_mismatches` counts mismatches where a or b is NaN or Inf.
+ * max_abs = max d and max_rel = max d/|B| (d > 0 and B = 0 give +Inf, d = 0
+ * and B = 0 give 0) over all pairs with both values finite; +0.0 if none.
+ * BITWISE mode: mismatches/first_mismatch equal the bitwise fields, the
+ * other fields are 0 / +0.0.
+ */
+typedef struct {
+  uint64_t mismatches;
+  int64_t first_mismatch;        /* logical index, -1 if none */
+  uint64_t bitwise_mismatches;   /* raw bits differ (always reported) */
+  int64_t first_bitwise;
+  uint64_t nonfinite_mismatches;
+  double max_abs, max_rel;
+} asmevo_segment_result;
+
+/*
+ * asmevo_diff_segments -- compares all n segments in one launch and writes
+ * results[0..n) (device memory).  Results are initialised in-stream, so n = 0
+ * and empty segments are fine.  Errors: ASMEVO_E_INVALID for null pointers,
+ * negative sizes, stride < cols, misaligned a/b, TOLERANCE on an integer
+ * dtype, negative or non-finite tolerances; ASMEVO_E_WORKSPACE.
+ */
+asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
+                                   asmevo_segment_result* results,
+                                   void* workspace, size_t ws_bytes, void* stream);
+
+/* As asmevo_diff_segments with an explicit number of workgroups (0 = the
+ * library's choice); results are identical for every value. */
+asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
+                                      asmevo_segment_result* results,
+                                      void* workspace, size_t ws_bytes, void* stream,
+                                      int32_t workgroups);
+
+/* Per-allocation guard result: counts of corrupted bytes and the lowest
+ * corrupted byte offset within each guard (-1 if intact). */
+typedef struct {
+  uint64_t bad_lo, bad_hi;
+  int64_t first_bad_lo, first_bad_hi;
+} asmevo_guard_result;
+
+/*
+ * asmevo_guard_check -- compares every guard byte of the n allocations
+ * against the canary regenerated from (seed, alloc_id) (the predicate iota
+ * of section 3.2 requires intact out-of-bounds guards), writing results[0..n)
+ * (device memory).  Only the allocation geometry (base, rows, cols, stride,
+ * guards, dtype, alloc_id) is used.  Errors: ASMEVO_E_INVALID,
+ * ASMEVO_E_WORKSPACE.
+ */
+asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
+                                 asmevo_guard_result* results,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes sufficient for any of the three calls with up to n_descs
+ * descriptors and n_inj injections. */
+size_t asmevo_workspace_bytes(int32_t n_descs, int64_t n_inj);
+const char* asmevo_status_string(asmevo_status status);
+int32_t asmevo_abi_version(void);
+/* hipError_t code of the last failing HIP call on this thread (0 if none). */
+int32_t asmevo_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,177 @@
+"""MI355X differential-oracle library: thin Python binding over libasmevo.so.
+
+The binding only marshals arguments (ctypes structures mirroring
+include/asmevo.h, device addresses from torch tensors, the current HIP
+stream); every step of the fill, comparison and guard check runs in the HIP
+kernels of the shared library.  Importing fails loudly if the library has
+not been built (`python -m paper_2608_20711_amd.build` or
+`__graft_entry__.build()`): there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libasmevo.so")
+
+# codes of include/asmevo.h
+OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, -1, -2, -3, -4
+F32, BF16, F16, FP8_E4M3, I32, I64, U8 = 1, 2, 3, 4, 5, 6, 7
+BITWISE, TOLERANCE = 0, 1
+NAN_EQUAL, NAN_STRICT = 0, 1
+DIST_NORMAL, DIST_UNIFORM_INT, DIST_BITS, DIST_CONST = 0, 1, 2, 3
+FILL_SATURATE = 1
+INJ_FLIP_BIT, INJ_STEP_WITHIN, INJ_SET_BEYOND, INJ_SET_NAN, INJ_SET_INF = 1, 2, 3, 4, 5
+INJ_GUARD_WRITE_LO, INJ_GUARD_WRITE_HI = 6, 7
+INJ_RATE = 0x100
+SIDE_CANDIDATE, SIDE_BOTH = 0, 1
+
+DTYPE_CODE = {"f32": F32, "bf16": BF16, "f16": F16, "fp8e4m3": FP8_E4M3, "i32": I32, "i64": I64, "u8": U8}
+MODE_CODE = {"bitwise": BITWISE, "tolerance": TOLERANCE}
+NAN_CODE = {"equal": NAN_EQUAL, "strict": NAN_STRICT}
+DIST_CODE = {"normal": DIST_NORMAL, "uniform_int": DIST_UNIFORM_INT, "bits": DIST_BITS, "const": DIST_CONST}
+KIND_CODE = {"flip_bit": INJ_FLIP_BIT, "step_within": INJ_STEP_WITHIN, "set_beyond": INJ_SET_BEYOND,
+             "set_nan": INJ_SET_NAN, "set_inf": INJ_SET_INF, "guard_write_lo": INJ_GUARD_WRITE_LO,
+             "guard_write_hi": INJ_GUARD_WRITE_HI}
+SIDE_CODE = {"candidate": SIDE_CANDIDATE, "both": SIDE_BOTH}
+
+
+class Alloc(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_uint64), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("stride", ctypes.c_int64), ("guard_lo", ctypes.c_int64), ("guard_hi", ctypes.c_int64),
+                ("dtype", ctypes.c_uint32), ("alloc_id", ctypes.c_uint32),
+                ("dist", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("p0", ctypes.c_double), ("p1", ctypes.c_double),
+                ("i0", ctypes.c_int64), ("i1", ctypes.c_int64)]
+
+
+class Injection(ctypes.Structure):
+    _fields_ = [("alloc", ctypes.c_uint32), ("kind", ctypes.c_uint32), ("sides", ctypes.c_uint32),
+                ("arg", ctypes.c_uint32), ("index", ctypes.c_int64),
+                ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_uint64), ("b", ctypes.c_uint64),
+                ("dtype", ctypes.c_uint32), ("mode", ctypes.c_uint32),
+                ("nan_policy", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("stride_a", ctypes.c_int64), ("stride_b", ctypes.c_int64),
+                ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
+class SegmentResult(ctypes.Structure):
+    _fields_ = [("mismatches", ctypes.c_uint64), ("first_mismatch", ctypes.c_int64),
+                ("bitwise_mismatches", ctypes.c_uint64), ("first_bitwise", ctypes.c_int64),
+                ("nonfinite_mismatches", ctypes.c_uint64),
+                ("max_abs", ctypes.c_double), ("max_rel", ctypes.c_double)]
+
+
+class GuardResult(ctypes.Structure):
+    _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
+                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
+
+
+SEGMENT_RESULT_FIELDS = [f for f, _ in SegmentResult._fields_]
+GUARD_RESULT_FIELDS = [f for f, _ in GuardResult._fields_]
+
+EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments_ex",
+            "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
+            "asmevo_abi_version", "asmevo_last_hip_error"]
+
+
+class AsmevoError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        self.status = status
+        msg = _lib().asmevo_status_string(status).decode()
+        if status == E_HIP:
+            msg += f" (hipError {_lib().asmevo_last_hip_error()})"
+        super().__init__(f"{call}: {msg} [{status}]")
+
+
+_handle: Optional[ctypes.CDLL] = None
+
+
+def _lib() -> ctypes.CDLL:
+    global _handle
+    if _handle is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2608_20711_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, P = ctypes.c_void_p, ctypes.POINTER
+        L.asmevo_fill_guarded.argtypes = [P(Alloc), ctypes.c_int32, P(Injection), ctypes.c_int64,
+                                          ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_size_t, vp]
+        L.asmevo_fill_guarded.restype = ctypes.c_int32
+        L.asmevo_diff_segments.argtypes = [P(Segment), ctypes.c_int32, vp, vp, ctypes.c_size_t, vp]
+        L.asmevo_diff_segments.restype = ctypes.c_int32
+        L.asmevo_diff_segments_ex.argtypes = [P(Segment), ctypes.c_int32, vp, vp, ctypes.c_size_t, vp,
+                                              ctypes.c_int32]
+        L.asmevo_diff_segments_ex.restype = ctypes.c_int32
+        L.asmevo_guard_check.argtypes = [P(Alloc), ctypes.c_int32, ctypes.c_uint64, vp, vp,
+                                         ctypes.c_size_t, vp]
+        L.asmevo_guard_check.restype = ctypes.c_int32
+        L.asmevo_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int64]
+        L.asmevo_workspace_bytes.restype = ctypes.c_size_t
+        L.asmevo_status_string.argtypes = [ctypes.c_int32]
+        L.asmevo_status_string.restype = ctypes.c_char_p
+        L.asmevo_abi_version.restype = ctypes.c_int32
+        L.asmevo_last_hip_error.restype = ctypes.c_int32
+        _handle = L
+    return _handle
+
+
+def lib() -> ctypes.CDLL:
+    return _lib()
+
+
+def _array(cls, items: Sequence):
+    arr = (cls * max(1, len(items)))()
+    for k, it in enumerate(items):
+        arr[k] = it
+    return arr
+
+
+def _check(status: int, call: str):
+    if status != OK:
+        raise AsmevoError(status, call)
+
+
+def workspace_bytes(n_descs: int, n_inj: int = 0) -> int:
+    return int(_lib().asmevo_workspace_bytes(n_descs, n_inj))
+
+
+def _stream_handle(stream) -> Optional[int]:
+    """A torch stream / raw handle / None -> hipStream_t as an int (None = default)."""
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream or None
+    if hasattr(stream, "cuda_stream"):
+        return stream.cuda_stream or None
+    return int(stream) or None
+
+
+def fill_guarded(allocs: Sequence[Alloc], injections: Sequence[Injection], seed: int, variant: int,
+                 workspace_ptr: int, workspace_size: int, stream=None) -> None:
+    a = _array(Alloc, allocs)
+    j = _array(Injection, injections)
+    _check(_lib().asmevo_fill_guarded(a, len(allocs), j, len(injections), seed, variant,
+                                      workspace_ptr, workspace_size, _stream_handle(stream)),
+           "asmevo_fill_guarded")
+
+
+def diff_segments(segments: Sequence[Segment], results_ptr: int, workspace_ptr: int,
+                  workspace_size: int, stream=None, workgroups: int = 0) -> None:
+    s = _array(Segment, segments)
+    _check(_lib().asmevo_diff_segments_ex(s, len(segments), results_ptr, workspace_ptr,
+                                          workspace_size, _stream_handle(stream), workgroups),
+           "asmevo_diff_segments")
+
+
+def guard_check(allocs: Sequence[Alloc], seed: int, results_ptr: int, workspace_ptr: int,
+                workspace_size: int, stream=None) -> None:
+    a = _array(Alloc, allocs)
+    _check(_lib().asmevo_guard_check(a, len(allocs), seed, results_ptr, workspace_ptr,
+                                     workspace_size, _stream_handle(stream)),
+           "asmevo_guard_check")

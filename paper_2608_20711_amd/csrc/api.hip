@@ -1,0 +1,362 @@
+// api.hip -- the C ABI (include/asmevo.h): argument validation, planning of
+// the device descriptor tables, one host-to-device copy into the caller's
+// workspace, kernel launches.  Validation finishes before anything is
+// enqueued, so an argument error leaves the stream untouched.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <vector>
+
+#include "asmevo.h"
+#include "kernels.h"
+#include "layout.h"
+
+using namespace asmevo;
+
+namespace {
+
+thread_local int32_t g_last_hip = 0;
+
+#define HIP_TRY(expr)                        \
+  do {                                       \
+    hipError_t e_ = (expr);                  \
+    if (e_ != hipSuccess) {                  \
+      g_last_hip = (int32_t)e_;              \
+      return ASMEVO_E_HIP;                   \
+    }                                        \
+  } while (0)
+
+int esize_of(uint32_t dtype) {
+  switch (dtype) {
+    case ASMEVO_F32: return 4;
+    case ASMEVO_BF16: return 2;
+    case ASMEVO_F16: return 2;
+    case ASMEVO_FP8_E4M3: return 1;
+    case ASMEVO_I32: return 4;
+    case ASMEVO_I64: return 8;
+    case ASMEVO_U8: return 1;
+    default: return 0;
+  }
+}
+
+bool is_float(uint32_t dtype) { return dtype >= ASMEVO_F32 && dtype <= ASMEVO_FP8_E4M3; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+uint64_t data_bytes(const asmevo_alloc& A) {
+  if (A.rows <= 0 || A.cols <= 0) return 0;
+  return (uint64_t)((A.rows - 1) * A.stride + A.cols) * (uint64_t)esize_of(A.dtype);
+}
+
+// Geometry checks shared by the fill and the guard check.
+asmevo_status check_alloc_geometry(const asmevo_alloc& A) {
+  const int es = esize_of(A.dtype);
+  if (es == 0) return ASMEVO_E_INVALID;
+  if (A.rows < 0 || A.cols < 0 || A.guard_lo < 0 || A.guard_hi < 0) return ASMEVO_E_INVALID;
+  if (A.rows > 0 && A.cols > 0 && A.stride < A.cols) return ASMEVO_E_INVALID;
+  if (A.guard_lo % es != 0) return ASMEVO_E_INVALID;
+  // keep every byte offset well inside 63 bits
+  const double approx = ((double)A.rows * (double)(A.stride > A.cols ? A.stride : A.cols) + 1.0) * es +
+                        (double)A.guard_lo + (double)A.guard_hi;
+  if (approx > 0x1p52) return ASMEVO_E_INVALID;
+  return ASMEVO_OK;
+}
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+template <typename T>
+void put(std::vector<uint8_t>& buf, size_t off, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(buf.data() + off, v.data(), v.size() * sizeof(T));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t asmevo_abi_version(void) { return ASMEVO_ABI_VERSION; }
+
+int32_t asmevo_last_hip_error(void) { return g_last_hip; }
+
+const char* asmevo_status_string(asmevo_status s) {
+  switch (s) {
+    case ASMEVO_OK: return "ok";
+    case ASMEVO_E_INVALID: return "invalid argument";
+    case ASMEVO_E_UNSUPPORTED: return "unsupported";
+    case ASMEVO_E_WORKSPACE: return "workspace missing or too small";
+    case ASMEVO_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t asmevo_workspace_bytes(int32_t n_descs, int64_t n_inj) {
+  const size_t n = n_descs > 0 ? (size_t)n_descs : 0;
+  const size_t m = n_inj > 0 ? (size_t)n_inj : 0;
+  return align256(n * sizeof(FillAlloc)) + align256(m * sizeof(FillRule)) +
+         align256(m * sizeof(PointEntry)) + align256(2 * n * sizeof(GuardRegion)) + 256;
+}
+
+// ---------------------------------------------------------------------------
+asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
+                                  const asmevo_injection* inj, int64_t n_inj, uint64_t seed,
+                                  uint32_t variant, void* workspace, size_t ws_bytes,
+                                  void* stream) {
+  if (n < 0 || n_inj < 0 || (n > 0 && !allocs) || (n_inj > 0 && !inj)) return ASMEVO_E_INVALID;
+  if (variant > 0xFFFFu) return ASMEVO_E_INVALID;
+  if (n == 0) return n_inj == 0 ? ASMEVO_OK : ASMEVO_E_INVALID;
+
+  // allocations
+  std::vector<FillAlloc> dev(n);
+  std::vector<std::pair<uint64_t, uint64_t>> spans;
+  uint64_t tiles = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    const asmevo_alloc& A = allocs[k];
+    asmevo_status st = check_alloc_geometry(A);
+    if (st != ASMEVO_OK) return st;
+    const int es = esize_of(A.dtype);
+    const uint64_t D = data_bytes(A);
+    const uint64_t total = (uint64_t)A.guard_lo + D + (uint64_t)A.guard_hi;
+    if (total > 0 && (A.base == 0 || (A.base & 15u) != 0)) return ASMEVO_E_INVALID;
+    if ((A.flags & ~ASMEVO_FILL_SATURATE) != 0) return ASMEVO_E_INVALID;
+    switch (A.dist) {
+      case ASMEVO_DIST_NORMAL:
+        if (!is_float(A.dtype) || !std::isfinite(A.p0) || !std::isfinite(A.p1)) return ASMEVO_E_INVALID;
+        break;
+      case ASMEVO_DIST_UNIFORM_INT:
+        if (A.i1 <= A.i0 || (uint64_t)(A.i1 - A.i0) > (1ull << 32)) return ASMEVO_E_INVALID;
+        break;
+      case ASMEVO_DIST_BITS:
+        break;
+      case ASMEVO_DIST_CONST:
+        if (is_float(A.dtype) && !std::isfinite(A.p0)) return ASMEVO_E_INVALID;
+        break;
+      default:
+        return ASMEVO_E_INVALID;
+    }
+    FillAlloc& F = dev[k];
+    std::memset(&F, 0, sizeof(F));
+    F.base = A.base;
+    F.total_bytes = total;
+    F.guard_lo = (uint64_t)A.guard_lo;
+    F.data_bytes = D;
+    F.rows = (uint64_t)A.rows;
+    F.cols = (uint64_t)A.cols;
+    F.stride = (uint64_t)A.stride;
+    F.tile_begin = tiles;
+    F.p0 = A.p0;
+    F.p1 = A.p1;
+    F.i0 = A.i0;
+    F.i1 = A.i1;
+    F.dtype = A.dtype;
+    F.esize = (uint32_t)es;
+    F.alloc_id = A.alloc_id;
+    F.dist = A.dist;
+    F.saturate = (A.flags & ASMEVO_FILL_SATURATE) ? 1u : 0u;
+    const uint64_t chunks = (total + kChunk - 1) / kChunk;
+    tiles += (chunks + kWave - 1) / kWave;
+    if (total) spans.emplace_back(A.base, A.base + total);
+  }
+  std::sort(spans.begin(), spans.end());
+  for (size_t s = 1; s < spans.size(); ++s)
+    if (spans[s].first < spans[s - 1].second) return ASMEVO_E_INVALID;
+
+  // injections: Bernoulli rules per allocation, deduplicated point entries
+  std::vector<std::vector<FillRule>> rules_of(n);
+  std::vector<uint32_t> rate_seen(n, 0);
+  std::vector<PointEntry> points;
+  std::map<std::pair<uint32_t, int64_t>, size_t> slot;   // (alloc, element) -> index in points
+  for (int64_t t = 0; t < n_inj; ++t) {
+    const asmevo_injection& J = inj[t];
+    if (J.alloc >= (uint32_t)n || J.sides > ASMEVO_SIDE_BOTH) return ASMEVO_E_INVALID;
+    const asmevo_alloc& A = allocs[J.alloc];
+    const int es = esize_of(A.dtype);
+    const bool rate = (J.kind & ASMEVO_INJ_RATE) != 0;
+    const uint32_t kind = J.kind & ~ASMEVO_INJ_RATE;
+    if (kind < ASMEVO_INJ_FLIP_BIT || kind > ASMEVO_INJ_GUARD_WRITE_HI) return ASMEVO_E_INVALID;
+    const bool guard = kind == ASMEVO_INJ_GUARD_WRITE_LO || kind == ASMEVO_INJ_GUARD_WRITE_HI;
+    if (guard && rate) return ASMEVO_E_INVALID;
+    if (!guard && kind != ASMEVO_INJ_FLIP_BIT && !is_float(A.dtype)) return ASMEVO_E_INVALID;
+    if (kind == ASMEVO_INJ_SET_INF && A.dtype == ASMEVO_FP8_E4M3) return ASMEVO_E_UNSUPPORTED;
+    if (kind == ASMEVO_INJ_FLIP_BIT && J.arg != 0xFFFFFFFFu && J.arg >= (uint32_t)(8 * es))
+      return ASMEVO_E_INVALID;
+    if (kind == ASMEVO_INJ_SET_BEYOND &&
+        (!std::isfinite(J.atol) || !std::isfinite(J.rtol) || J.atol < 0 || J.rtol < 0))
+      return ASMEVO_E_INVALID;
+    const bool applies = variant != 0 || J.sides == ASMEVO_SIDE_BOTH;
+    const uint32_t vsel = J.sides == ASMEVO_SIDE_BOTH ? 0u : variant;
+    if (rate) {
+      if (J.index < 0 || J.index > (int64_t)(1ll << 32)) return ASMEVO_E_INVALID;
+      const uint32_t ordinal = rate_seen[J.alloc]++;
+      if (ordinal >= (uint32_t)kMaxRules) return ASMEVO_E_UNSUPPORTED;
+      if (applies)
+        rules_of[J.alloc].push_back(FillRule{kind, vsel, J.arg, ordinal, (uint64_t)J.index, J.atol, J.rtol});
+      continue;
+    }
+    if (guard) {
+      const int64_t gsize = kind == ASMEVO_INJ_GUARD_WRITE_LO ? A.guard_lo : A.guard_hi;
+      if (J.index < 0 || J.index + (int64_t)J.arg > gsize) return ASMEVO_E_INVALID;
+      if (applies && J.arg > 0)
+        points.push_back(PointEntry{J.alloc, kind, vsel, J.arg, J.index, J.atol, J.rtol});
+      continue;
+    }
+    if (J.index < 0 || J.index >= A.rows * A.cols) return ASMEVO_E_INVALID;
+    if (!applies) continue;
+    const PointEntry P{J.alloc, kind, vsel, J.arg, J.index, J.atol, J.rtol};
+    const auto key = std::make_pair(J.alloc, J.index);
+    auto it = slot.find(key);
+    if (it != slot.end()) {
+      points[it->second] = P;                       // a later entry overrides
+    } else {
+      slot.emplace(key, points.size());
+      points.push_back(P);
+    }
+  }
+  std::vector<FillRule> rules;
+  for (int32_t k = 0; k < n; ++k) {
+    dev[k].rule_begin = (uint32_t)rules.size();
+    dev[k].rule_count = (uint32_t)rules_of[k].size();
+    rules.insert(rules.end(), rules_of[k].begin(), rules_of[k].end());
+  }
+
+  // staging
+  const size_t off_rules = align256(dev.size() * sizeof(FillAlloc));
+  const size_t off_pts = off_rules + align256(rules.size() * sizeof(FillRule));
+  const size_t bytes = off_pts + points.size() * sizeof(PointEntry);
+  if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  std::vector<uint8_t> host(bytes, 0);
+  put(host, 0, dev);
+  put(host, off_rules, rules);
+  put(host, off_pts, points);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemcpyAsync(workspace, host.data(), bytes, hipMemcpyHostToDevice, s));
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  const FillAlloc* d_allocs = reinterpret_cast<const FillAlloc*>(ws);
+  const FillRule* d_rules = reinterpret_cast<const FillRule*>(ws + off_rules);
+  const PointEntry* d_pts = reinterpret_cast<const PointEntry*>(ws + off_pts);
+  const uint64_t waves = std::max<uint64_t>(1, std::min<uint64_t>(tiles, (uint64_t)device_cus() * 32));
+  const int wg = (int)((waves + (kFillBlock / kWave) - 1) / (kFillBlock / kWave));
+  HIP_TRY(launch_fill(d_allocs, n, d_rules, tiles, seed, wg, s));
+  HIP_TRY(launch_inject(d_allocs, d_pts, (int)points.size(), seed, s));
+  return ASMEVO_OK;
+}
+
+// ---------------------------------------------------------------------------
+asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
+                                      asmevo_segment_result* results, void* workspace,
+                                      size_t ws_bytes, void* stream, int32_t workgroups) {
+  if (n < 0 || (n > 0 && (!segs || !results)) || workgroups < 0) return ASMEVO_E_INVALID;
+  if (n == 0) return ASMEVO_OK;
+  std::vector<DiffSeg> dev(n);
+  uint64_t tiles = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    const asmevo_segment& S = segs[k];
+    const int es = esize_of(S.dtype);
+    if (es == 0) return ASMEVO_E_INVALID;
+    if (S.mode != ASMEVO_BITWISE && S.mode != ASMEVO_TOLERANCE) return ASMEVO_E_INVALID;
+    if (S.nan_policy != ASMEVO_NAN_EQUAL && S.nan_policy != ASMEVO_NAN_STRICT) return ASMEVO_E_INVALID;
+    if (S.rows < 0 || S.cols < 0) return ASMEVO_E_INVALID;
+    const bool empty = S.rows == 0 || S.cols == 0;
+    if (!empty) {
+      if (S.stride_a < S.cols || S.stride_b < S.cols) return ASMEVO_E_INVALID;
+      if (!S.a || !S.b || (S.a % (uint64_t)es) != 0 || (S.b % (uint64_t)es) != 0) return ASMEVO_E_INVALID;
+      const double span = (double)S.rows * (double)std::max(S.stride_a, S.stride_b) * es;
+      if (span > 0x1p52) return ASMEVO_E_INVALID;
+    }
+    if (S.mode == ASMEVO_TOLERANCE) {
+      if (!is_float(S.dtype)) return ASMEVO_E_INVALID;
+      if (!std::isfinite(S.atol) || !std::isfinite(S.rtol) || S.atol < 0 || S.rtol < 0)
+        return ASMEVO_E_INVALID;
+    }
+    DiffSeg& D = dev[k];
+    std::memset(&D, 0, sizeof(D));
+    D.a = S.a;
+    D.b = S.b;
+    D.atol = S.atol;
+    D.rtol = S.rtol;
+    D.dtype = S.dtype;
+    D.mode = S.mode;
+    D.esize = (uint32_t)es;
+    D.result_index = (uint32_t)k;
+    D.tile_begin = tiles;
+    if (!empty) {
+      const bool flat = S.rows == 1 || (S.stride_a == S.cols && S.stride_b == S.cols);
+      D.rows = flat ? 1 : (uint64_t)S.rows;
+      D.cols = flat ? (uint64_t)(S.rows * S.cols) : (uint64_t)S.cols;
+      D.a_pitch = (uint64_t)S.stride_a * es;
+      D.b_pitch = (uint64_t)S.stride_b * es;
+      D.row_bytes = D.cols * es;
+      D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
+      const bool aligned = (S.a % 16 == 0) && (S.b % 16 == 0) &&
+                           (D.rows == 1 || (D.a_pitch % 16 == 0 && D.b_pitch % 16 == 0));
+      D.flags = (aligned ? kSegVec : 0u) | ((D.row_bytes % kChunk) ? kSegTail : 0u) |
+                ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
+      const uint64_t chunks = D.rows * D.row_chunks;
+      D.tile_count = (chunks + kTileChunks - 1) / kTileChunks;
+      tiles += D.tile_count;
+    }
+  }
+  const size_t bytes = dev.size() * sizeof(DiffSeg);
+  if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
+  int wg = workgroups;
+  if (wg == 0) wg = device_cus() * 4;          // 16 waves per CU
+  HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(workspace), n, tiles, results, wg, s));
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
+                                   asmevo_segment_result* results, void* workspace,
+                                   size_t ws_bytes, void* stream) {
+  return asmevo_diff_segments_ex(segs, n, results, workspace, ws_bytes, stream, 0);
+}
+
+// ---------------------------------------------------------------------------
+asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
+                                 asmevo_guard_result* results, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  if (n < 0 || (n > 0 && (!allocs || !results))) return ASMEVO_E_INVALID;
+  if (n == 0) return ASMEVO_OK;
+  std::vector<GuardRegion> regs;
+  uint64_t chunks = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    const asmevo_alloc& A = allocs[k];
+    asmevo_status st = check_alloc_geometry(A);
+    if (st != ASMEVO_OK) return st;
+    if ((A.guard_lo > 0 || A.guard_hi > 0) && A.base == 0) return ASMEVO_E_INVALID;
+    const uint64_t D = data_bytes(A);
+    for (uint32_t side = 0; side < 2; ++side) {
+      const uint64_t g = (uint64_t)(side ? A.guard_hi : A.guard_lo);
+      if (g == 0) continue;
+      GuardRegion R;
+      std::memset(&R, 0, sizeof(R));
+      R.addr = side ? A.base + (uint64_t)A.guard_lo + D : A.base;
+      R.bytes = g;
+      R.chunk_begin = chunks;
+      R.alloc_id = A.alloc_id;
+      R.side = side;
+      R.result_index = (uint32_t)k;
+      regs.push_back(R);
+      chunks += (g + kChunk - 1) / kChunk;
+    }
+  }
+  const size_t bytes = std::max<size_t>(regs.size(), 1) * sizeof(GuardRegion);
+  if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!regs.empty())
+    HIP_TRY(hipMemcpyAsync(workspace, regs.data(), regs.size() * sizeof(GuardRegion),
+                           hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_guard(reinterpret_cast<const GuardRegion*>(workspace), (int)regs.size(), chunks,
+                       seed, results, n, s));
+  return ASMEVO_OK;
+}
+
+}  // extern "C"

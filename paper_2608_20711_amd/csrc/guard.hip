@@ -1,0 +1,86 @@
+// guard.hip -- canary integrity check of guard regions (AsmEvo section 3.2:
+// the predicate iota requires intact out-of-bounds guards; section 3.4:
+// Tier-1 allocations carry canary-initialised guards, and guard regions are
+// checked byte-exactly).  The expected bytes are regenerated from
+// (seed, alloc_id, side), so only the candidate's guard bytes are read.
+#include "device_math.h"
+#include "kernels.h"
+#include "layout.h"
+
+namespace asmevo {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ void guard_init_kernel(asmevo_guard_result* results, int n) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n) return;
+  asmevo_guard_result r;
+  r.bad_lo = 0;
+  r.bad_hi = 0;
+  r.first_bad_lo = -1;
+  r.first_bad_hi = -1;
+  results[t] = r;
+}
+
+// One thread per 16 guard bytes; the chunk's region is found by binary search
+// over the regions' chunk prefix.
+__global__ __launch_bounds__(256) void guard_kernel(const GuardRegion* __restrict__ regs, int n,
+                                                    uint64_t total_chunks, uint64_t seed,
+                                                    asmevo_guard_result* results) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total_chunks; g += stride) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (regs[mid].chunk_begin <= g) lo = mid;
+      else hi = mid - 1;
+    }
+    const GuardRegion R = regs[lo];
+    const uint64_t p0 = (g - R.chunk_begin) * kChunk;
+    const uint64_t left = R.bytes - p0;
+    const uint32_t nb = left < (uint64_t)kChunk ? (uint32_t)left : (uint32_t)kChunk;
+    const U4 C = stream(seed, R.alloc_id, kCanary, R.side, 0, p0 >> 4);
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(R.addr) + p0;
+    uint32_t mask = 0;
+    if (nb == (uint32_t)kChunk && (reinterpret_cast<uintptr_t>(src) & 15u) == 0) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+      const uint32_t x[4] = {v.x ^ C.x, v.y ^ C.y, v.z ^ C.z, v.w ^ C.w};
+#pragma unroll
+      for (int k = 0; k < 16; ++k) mask |= ((x[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? (1u << k) : 0u;
+    } else {
+      for (uint32_t k = 0; k < nb; ++k)
+        mask |= (src[k] != byte_of(C, k)) ? (1u << k) : 0u;
+    }
+    if (mask) {
+      asmevo_guard_result* res = results + R.result_index;
+      const uint64_t cnt = (uint64_t)__builtin_popcount(mask);
+      const uint64_t first = p0 + (uint64_t)__builtin_ctz(mask);
+      if (R.side == 0) {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&res->bad_lo), cnt);
+        atomicMin(reinterpret_cast<unsigned long long*>(&res->first_bad_lo), first);
+      } else {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&res->bad_hi), cnt);
+        atomicMin(reinterpret_cast<unsigned long long*>(&res->first_bad_hi), first);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_guard(const GuardRegion* regs, int n_regs, uint64_t total_chunks, uint64_t seed,
+                        asmevo_guard_result* results, int n_results, hipStream_t stream) {
+  if (n_results == 0) return hipSuccess;
+  hipLaunchKernelGGL(guard_init_kernel, dim3((n_results + 255) / 256), dim3(256), 0, stream,
+                     results, n_results);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || total_chunks == 0) return e;
+  uint64_t blocks = (total_chunks + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(guard_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, regs, n_regs,
+                     total_chunks, seed, results);
+  return hipGetLastError();
+}
+
+}  // namespace asmevo

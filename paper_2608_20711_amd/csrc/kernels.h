@@ -1,0 +1,22 @@
+// kernels.h -- host-side launchers of the library's kernels (internal).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "asmevo.h"
+#include "layout.h"
+
+namespace asmevo {
+
+hipError_t launch_fill(const FillAlloc* allocs, int n, const FillRule* rules, uint64_t total_tiles,
+                       uint64_t seed, int workgroups, hipStream_t stream);
+hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_pts, uint64_t seed,
+                         hipStream_t stream);
+
+hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
+                       asmevo_segment_result* results, int workgroups, hipStream_t stream);
+
+hipError_t launch_guard(const GuardRegion* regs, int n_regs, uint64_t total_chunks, uint64_t seed,
+                        asmevo_guard_result* results, int n_results, hipStream_t stream);
+
+}  // namespace asmevo

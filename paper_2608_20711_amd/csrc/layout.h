@@ -1,0 +1,79 @@
+// layout.h -- device-side descriptor tables staged by the host planner into
+// the caller's workspace.  Internal to the library (not part of the C ABI).
+#pragma once
+#include <stdint.h>
+
+namespace asmevo {
+
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kChunk = 16;         // bytes per lane per load (dwordx4)
+
+// ---------------------------------------------------------------- diff
+constexpr int kDiffUnroll = 8;                       // chunks per lane per tile
+constexpr int kTileChunks = kWave * kDiffUnroll;     // 512 chunks = 8 KiB per side
+constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
+
+enum : uint32_t {
+  kSegVec = 1u,       // a, b and both row pitches are 16-byte aligned
+  kSegTail = 2u,      // row bytes not a multiple of 16: last chunk of a row is partial
+  kSegStrict = 4u,    // TOLERANCE with the strict NaN policy
+};
+
+struct DiffSeg {                // 128 bytes
+  uint64_t a, b;                // element (0,0) of candidate / reference
+  uint64_t a_pitch, b_pitch;    // bytes between row starts
+  uint64_t rows;                // 1 when the segment is contiguous in both operands
+  uint64_t cols;                // logical elements per (possibly flattened) row
+  uint64_t row_bytes;           // cols * esize
+  uint64_t row_chunks;          // ceil(row_bytes / 16)
+  uint64_t tile_begin;          // first tile of this segment in the global tile space
+  uint64_t tile_count;
+  double atol, rtol;
+  uint32_t dtype, mode, flags, esize;
+  uint32_t result_index, pad0, pad1, pad2;
+};
+static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
+
+// ---------------------------------------------------------------- fill
+constexpr int kMaxRules = 16;      // Bernoulli rules per allocation
+constexpr int kFillBlock = 256;
+
+struct FillAlloc {              // 128 bytes
+  uint64_t base;                // first lo-guard byte (16-byte aligned)
+  uint64_t total_bytes;         // guard_lo + data + guard_hi
+  uint64_t guard_lo, data_bytes;
+  uint64_t rows, cols, stride;  // elements
+  uint64_t tile_begin;          // first 64-chunk tile of this allocation
+  double p0, p1;
+  int64_t i0, i1;
+  uint32_t dtype, esize, alloc_id, dist;
+  uint32_t saturate, rule_begin, rule_count, pad0;
+};
+static_assert(sizeof(FillAlloc) == 128, "FillAlloc layout");
+
+struct FillRule {               // a Bernoulli rule (or a point entry)
+  uint32_t kind, vsel, arg, ordinal;   // vsel: variant field used in SELECT/INJECT counters
+  uint64_t threshold;           // RATE: selected iff draw < threshold
+  double atol, rtol;
+};
+static_assert(sizeof(FillRule) == 40, "FillRule layout");
+
+struct PointEntry {             // one deduplicated point injection
+  uint32_t alloc, kind, vsel, arg;
+  int64_t index;
+  double atol, rtol;
+};
+static_assert(sizeof(PointEntry) == 40, "PointEntry layout");
+
+// ---------------------------------------------------------------- guard
+struct GuardRegion {            // one guard side of one allocation
+  uint64_t addr;                // first guard byte
+  uint64_t bytes;
+  uint64_t chunk_begin;         // first 16-byte chunk in the global chunk space
+  uint32_t alloc_id, side;      // side 0 = lo, 1 = hi
+  uint32_t result_index, pad0;
+  uint32_t pad1, pad2;
+};
+static_assert(sizeof(GuardRegion) == 48, "GuardRegion layout");
+
+}  // namespace asmevo

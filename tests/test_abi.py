@@ -1,0 +1,164 @@
+"""CPU-side checks of the C ABI: the shared library loads, exports every
+function include/asmevo.h declares, the ctypes structures of the binding have
+the header's layout (checked by compiling the header with gcc), and argument
+errors are reported before anything touches the GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_20711_amd as lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "asmevo.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(asmevo_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = lib.lib()
+    declared = _declared_functions()
+    assert declared == sorted(lib.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", lib.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    for name in declared:
+        assert re.search(rf"\bT {name}\b", out), f"{name} not exported"
+
+
+def test_struct_layouts_match_header(tmp_path):
+    src = tmp_path / "layout.c"
+    fields = {
+        "asmevo_alloc": lib.Alloc, "asmevo_injection": lib.Injection, "asmevo_segment": lib.Segment,
+        "asmevo_segment_result": lib.SegmentResult, "asmevo_guard_result": lib.GuardResult,
+    }
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "asmevo.h"', "int main(void) {"]
+    for cname, cls in fields.items():
+        lines.append(f'  printf("{cname} %zu\\n", sizeof({cname}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{cname}.{f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["  return 0;", "}"]
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-I", os.path.dirname(HEADER), str(src), "-o",
+                    str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                 check=True).stdout.splitlines())
+    for cname, cls in fields.items():
+        assert int(got[cname]) == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert int(got[f"{cname}.{f}"]) == getattr(cls, f).offset, f"{cname}.{f}"
+    assert ctypes.sizeof(lib.SegmentResult) == 56
+
+
+def test_version_status_strings_workspace():
+    L = lib.lib()
+    assert L.asmevo_abi_version() == 1
+    for st in (lib.OK, lib.E_INVALID, lib.E_UNSUPPORTED, lib.E_WORKSPACE, lib.E_HIP):
+        assert L.asmevo_status_string(st)
+    assert lib.workspace_bytes(4096, 0) >= 4096 * 128
+    assert lib.workspace_bytes(0, 0) > 0
+
+
+def _seg(**kw):
+    d = dict(a=0x10000, b=0x20000, dtype=lib.F32, mode=lib.TOLERANCE, nan_policy=0, reserved=0,
+             rows=1, cols=8, stride_a=8, stride_b=8, atol=0.0, rtol=0.0)
+    d.update(kw)
+    return lib.Segment(**d)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(dtype=99), dict(mode=7), dict(nan_policy=3), dict(rows=-1), dict(cols=-2),
+    dict(stride_a=4), dict(stride_b=7), dict(a=0), dict(b=0), dict(a=0x10001), dict(b=0x20002),
+    dict(dtype=lib.I32, mode=lib.TOLERANCE), dict(atol=-1.0), dict(rtol=float("nan")),
+    dict(atol=float("inf")),
+])
+def test_diff_argument_errors_before_any_device_work(bad):
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments([_seg(**bad)], 0x40000, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+
+
+def test_diff_null_results_and_workspace():
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments([_seg()], 0, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments([_seg()], 0x40000, 0x50000, 16, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments([_seg()], 0x40000, 0, 1 << 20, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
+
+
+def _alloc(**kw):
+    d = dict(base=0x100000, rows=1, cols=64, stride=64, guard_lo=16, guard_hi=16, dtype=lib.F32,
+             alloc_id=0, dist=lib.DIST_NORMAL, flags=0, p0=0.0, p1=1.0, i0=0, i1=0)
+    d.update(kw)
+    return lib.Alloc(**d)
+
+
+def _inj(**kw):
+    d = dict(alloc=0, kind=lib.INJ_FLIP_BIT, sides=0, arg=0, index=0, atol=0.0, rtol=0.0)
+    d.update(kw)
+    return lib.Injection(**d)
+
+
+@pytest.mark.parametrize("allocs,inj,status", [
+    ([_alloc(base=0x100008)], [], lib.E_INVALID),                         # not 16-byte aligned
+    ([_alloc(base=0)], [], lib.E_INVALID),
+    ([_alloc(dtype=0)], [], lib.E_INVALID),
+    ([_alloc(stride=10)], [], lib.E_INVALID),
+    ([_alloc(guard_lo=6)], [], lib.E_INVALID),                            # not a multiple of 4
+    ([_alloc(dist=9)], [], lib.E_INVALID),
+    ([_alloc(dtype=lib.I32)], [], lib.E_INVALID),                         # normal on an integer dtype
+    ([_alloc(dist=lib.DIST_UNIFORM_INT, i0=5, i1=5)], [], lib.E_INVALID),
+    ([_alloc(dist=lib.DIST_UNIFORM_INT, i0=0, i1=(1 << 32) + 1)], [], lib.E_INVALID),
+    ([_alloc(p1=float("inf"))], [], lib.E_INVALID),
+    ([_alloc(flags=2)], [], lib.E_INVALID),
+    ([_alloc(), _alloc(base=0x100100, alloc_id=1)], [], lib.E_INVALID),   # overlapping allocations
+    ([_alloc()], [_inj(alloc=1)], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=9)], lib.E_INVALID),
+    ([_alloc()], [_inj(index=64)], lib.E_INVALID),
+    ([_alloc()], [_inj(arg=32)], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=lib.INJ_GUARD_WRITE_LO, index=10, arg=7)], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=lib.INJ_GUARD_WRITE_HI | lib.INJ_RATE, index=1)], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=lib.INJ_FLIP_BIT | lib.INJ_RATE, index=(1 << 32) + 1)], lib.E_INVALID),
+    ([_alloc(dtype=lib.I32, dist=lib.DIST_UNIFORM_INT, i1=9)], [_inj(kind=lib.INJ_SET_NAN)], lib.E_INVALID),
+    ([_alloc(dtype=lib.FP8_E4M3)], [_inj(kind=lib.INJ_SET_INF)], lib.E_UNSUPPORTED),
+    ([_alloc()], [_inj(kind=lib.INJ_SET_BEYOND, atol=-1.0)], lib.E_INVALID),
+    ([_alloc()], [_inj(sides=2)], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=lib.INJ_FLIP_BIT | lib.INJ_RATE, index=10)] * 17, lib.E_UNSUPPORTED),
+])
+def test_fill_argument_errors_before_any_device_work(allocs, inj, status):
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.fill_guarded(allocs, inj, 1, 1, 0x900000, 1 << 20, stream=0)
+    assert e.value.status == status
+
+
+def test_fill_variant_range_and_workspace():
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.fill_guarded([_alloc()], [], 1, 1 << 16, 0x900000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.fill_guarded([_alloc()], [], 1, 0, 0x900000, 8, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
+
+
+def test_guard_argument_errors():
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.guard_check([_alloc(stride=3)], 1, 0x40000, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.guard_check([_alloc()], 1, 0, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.guard_check([_alloc()], 1, 0x40000, 0x50000, 4, stream=0)
+    assert e.value.status == lib.E_WORKSPACE

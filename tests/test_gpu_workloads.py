@@ -1,0 +1,110 @@
+"""GPU parity on the five seeded workloads: the HIP fill, diff and guard check
+against the CPU oracle, bit for bit on every output (fill bytes, counts,
+first indices, fp64 maxima, guard counts and offsets).
+
+Reduced sizes check every byte and every result; full sizes check every
+comparison and guard result against the oracle run on the GPU's own buffers,
+plus sampled windows of the fills; the 4096-buffer sweep checks sampled
+segments and the properties that hold at any size."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_helpers import (THREADS, assert_fill_equal, assert_results_equal, check_fill_sampled, log,
+                         run_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name", list(workloads.ALL))
+def test_reduced_size_everything_bit_exact(name):
+    w = workloads.ALL[name](small=True)
+    log(f"[reduced] {name}: {len(w.allocs)} allocs, {w.arena_bytes} B per side")
+    st = run_gpu(w)
+    P = oracle.Prepared(w)
+    ref = P.fill_arena(0, THREADS)
+    cand = P.fill_arena(1, THREADS)
+    assert_fill_equal(w, st.arena_host("ref"), ref, f"{name} reference fill")
+    assert_fill_equal(w, st.arena_host("cand"), cand, f"{name} candidate fill")
+    assert_results_equal(st.seg_results(), oracle.diff_workload(w, cand, ref, THREADS), f"{name} diff")
+    assert_results_equal(st.guard_results(), oracle.guard_workload(w, cand), f"{name} guard")
+
+
+@pytest.mark.parametrize("name", ["single_fp32", "padded_bf16", "decode_state", "int_lowp"])
+def test_full_size_bit_exact(name):
+    w = workloads.ALL[name]()
+    log(f"[full] {name}: {w.arena_bytes} B per side")
+    st = run_gpu(w)
+    cand = st.arena_host("cand")
+    ref = st.arena_host("ref")
+    # every comparison / guard result against the oracle on the same bytes
+    assert_results_equal(st.seg_results(), oracle.diff_workload(w, cand, ref, THREADS), f"{name} diff")
+    assert_results_equal(st.guard_results(), oracle.guard_workload(w, cand), f"{name} guard")
+    # the fills themselves, sampled (whole allocation when it is small)
+    rng = np.random.default_rng(12)
+    if w.arena_bytes <= (16 << 20):
+        P = oracle.Prepared(w)
+        assert_fill_equal(w, ref, P.fill_arena(0, THREADS), f"{name} reference fill")
+        assert_fill_equal(w, cand, P.fill_arena(1, THREADS), f"{name} candidate fill")
+    else:
+        check_fill_sampled(w, st, {"ref": 0, "cand": 1}, rng, n_random=24)
+    del cand, ref
+
+
+def test_sweep_full_size_sampled():
+    """4096 buffers, ~64 GiB per side, in the launch configuration the bench
+    times: sampled segments bit-exact against the oracle, every guard intact,
+    and the flip count consistent with the 1e-6 rate."""
+    w = workloads.sweep()
+    free, total = torch.cuda.mem_get_info()
+    need = 2 * w.arena_bytes + (1 << 30)
+    if free < need:
+        pytest.skip(f"needs {need >> 30} GiB of free device memory, {free >> 30} GiB free")
+    log(f"[sweep] {len(w.allocs)} buffers, {w.arena_bytes / 2**30:.1f} GiB per side")
+    st = run_gpu(w)
+    res = st.seg_results()
+    guards = st.guard_results()
+    assert all(g == {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1} for g in guards)
+    n_el = sum(a.n_elements for a in w.allocs)
+    total_bw = sum(r["bitwise_mismatches"] for r in res)
+    assert abs(total_bw - 1e-6 * n_el) < 6 * math.sqrt(1e-6 * n_el)
+    for r in res:
+        assert r["mismatches"] <= r["bitwise_mismatches"]
+    rng = np.random.default_rng(5)
+    order = np.argsort([a.total_bytes for a in w.allocs])
+    sample = list(order[:8]) + list(order[-4:]) + list(rng.choice(len(w.allocs), 20, replace=False))
+    P = oracle.Prepared(w)
+    for k in sorted(set(int(s) for s in sample)):
+        a = w.allocs[k]
+        cand_k = st.alloc_bytes("cand", k)
+        ref_k = st.alloc_bytes("ref", k)
+        c = w.compares[k]
+        want = oracle.diff_segment(a.dtype, c.mode, c.nan_policy, a.rows, a.cols, a.stride, a.stride,
+                                   c.atol, c.rtol, cand_k, ref_k, a.guard_lo, a.guard_lo)
+        assert_results_equal([res[k]], [want], f"sweep segment {k} ({a.dtype}, {a.data_bytes} B)")
+        # fill windows of this allocation
+        for s, n in [(0, min(a.total_bytes, 2048)), (max(0, a.total_bytes - 2048), min(a.total_bytes, 2048))]:
+            assert np.array_equal(cand_k[s:s + n], P.fill_range(k, 1, s, n)), f"cand fill {k}"
+            assert np.array_equal(ref_k[s:s + n], P.fill_range(k, 0, s, n)), f"ref fill {k}"
+        # every flipped element of this buffer is a single-bit difference from the reference fill
+        log(f"  segment {k}: {a.dtype} {a.data_bytes} B ok ({res[k]['bitwise_mismatches']} flips)")
+    del st
+    torch.cuda.empty_cache()
+
+
+def test_repeats_and_launch_geometry_are_bit_identical():
+    """The check is repeated three times per candidate (section 4.1); results
+    must not depend on repetition or on the number of workgroups."""
+    w = workloads.padded_bf16(small=True)
+    st = run_gpu(w)
+    base = st.seg_results()
+    for rep in range(3):
+        st.diff()
+        assert st.seg_results() == base
+    for wg in (1, 2, 3, 17, 64, 1000, 4096):
+        st.diff(workgroups=wg)
+        assert st.seg_results() == base, f"workgroups={wg}"
