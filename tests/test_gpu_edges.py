@@ -19,10 +19,19 @@ pytestmark = pytest.mark.gpu
 _NP = {1: np.uint8, 2: np.uint16, 4: np.uint32, 8: np.uint64}
 
 
+def _extent(s, stride):
+    if s["rows"] == 0 or s["cols"] == 0:
+        return 0
+    return ((s["rows"] - 1) * stride + s["cols"]) * ESIZE[s["dtype"]]
+
+
 def _gpu_diff(seg_specs, a_dev, b_dev, workgroups=0):
     """seg_specs: list of dicts with dtype/mode/policy/rows/cols/sa/sb/atol/rtol/a_off/b_off."""
     segs = []
     for s in seg_specs:
+        # every byte a segment names must lie inside the buffers (checked before launch)
+        assert s["a_off"] + _extent(s, s["sa"]) <= a_dev.numel(), s
+        assert s["b_off"] + _extent(s, s["sb"]) <= b_dev.numel(), s
         segs.append(lib.Segment(a_dev.data_ptr() + s["a_off"], b_dev.data_ptr() + s["b_off"],
                                 lib.DTYPE_CODE[s["dtype"]], lib.MODE_CODE[s["mode"]],
                                 lib.NAN_CODE[s["policy"]], 0, s["rows"], s["cols"], s["sa"], s["sb"],
@@ -105,8 +114,10 @@ def test_random_patterns_all_layouts(dtype):
         specs.append(_spec(dtype, 1, n, n, n, 0, 0, policy=policy))                      # contiguous, aligned
     specs.append(_spec(dtype, 1, n - 7, n, n, es, 3 * es))                               # misaligned a and b
     specs.append(_spec(dtype, 1, 10_007, 10_007, 10_007, 16, 16))                        # ragged tail
-    specs.append(_spec(dtype, 999, 1000, 1024, 1024, 0, 0))                              # 2-D, 16-B pitches
-    specs.append(_spec(dtype, 333, 1001, 1003, 1009, 0, es, policy="strict"))            # 2-D ragged, misaligned
+    rows2d = min(999, n // 1024 - 1)
+    specs.append(_spec(dtype, rows2d, 1000, 1024, 1024, 0, 0))                           # 2-D, 16-B pitches
+    rows3 = min(333, n // 1009 - 1)
+    specs.append(_spec(dtype, rows3, 1001, 1003, 1009, 0, es, policy="strict"))          # 2-D ragged, misaligned
     specs.append(_spec(dtype, 4, 3, 5, 3, 32, 64))                                       # tiny 2-D
     specs.append(_spec(dtype, 1, 1, 1, 1, es * 5, es * 9))                               # one element
     specs.append(_spec(dtype, 0, 10, 10, 10, 0, 0))                                      # empty
