@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--cpu-sample-bytes", type=float, default=1.5 * 2 ** 30,
                    help="logical bytes per side of the oracle's sample")
     p.add_argument("--workgroups", type=int, default=0)
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                   help="first copy BYTES device-to-device with torch (a plain copy kernel of known "
+                        "size, to scale HBM traffic counters)")
     return p.parse_args()
 
 
@@ -100,6 +103,14 @@ def main():
     from paper_2608_20711_amd.state import DeviceState
 
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     w = workloads.ALL[args.workload](small=args.small)
     print(f"# workload {w.name}: {len(w.allocs)} buffers, {w.arena_bytes / 2**30:.2f} GiB per side",
           file=sys.stderr, flush=True)

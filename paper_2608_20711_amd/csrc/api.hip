@@ -294,12 +294,22 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
       D.b_pitch = (uint64_t)S.stride_b * es;
       D.row_bytes = D.cols * es;
       D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
+      D.full_chunks = D.row_bytes / kChunk;
       const bool aligned = (S.a % 16 == 0) && (S.b % 16 == 0) &&
                            (D.rows == 1 || (D.a_pitch % 16 == 0 && D.b_pitch % 16 == 0));
-      D.flags = (aligned ? kSegVec : 0u) | ((D.row_bytes % kChunk) ? kSegTail : 0u) |
+      const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
+      D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) |
                 ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
-      const uint64_t chunks = D.rows * D.row_chunks;
-      D.tile_count = (chunks + kTileChunks - 1) / kTileChunks;
+      if (narrow) {
+        D.tiles_per_row = 0;
+        D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
+      } else {
+        const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;
+        D.tile_count = D.rows * tpr;
+        // 2-D row-tiled segments index tiles in 32 bits
+        if (D.rows > 1 && (D.tile_count >> 32) != 0) return ASMEVO_E_INVALID;
+        D.tiles_per_row = (uint32_t)(tpr > 0xFFFFFFFFull ? 0xFFFFFFFFull : tpr);
+      }
       tiles += D.tile_count;
     }
   }

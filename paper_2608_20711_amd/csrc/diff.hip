@@ -182,84 +182,103 @@ __device__ __forceinline__ u32x4 ld_nt(const uint8_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 
+// Chunk pair of a row whose bytes [c*16, c*16 + nbytes) are valid: a vector
+// load when the chunk is whole and aligned, element loads otherwise.
 template <int DT>
-__device__ __forceinline__ void diff_tile(const DiffSeg& S, uint64_t tile, uint32_t lane, Acc& acc) {
+__device__ __forceinline__ void load_chunk(const uint8_t* pa, const uint8_t* pb, uint32_t nbytes,
+                                           bool vec, u32x4& va, u32x4& vb) {
+  if (nbytes == (uint32_t)kChunk && vec) {
+    va = ld_nt(pa);
+    vb = ld_nt(pb);
+  } else {
+    const uint32_t nv = nbytes / Et<DT>::es;
+    va = load_elems<DT>(pa, nv);
+    vb = load_elems<DT>(pb, nv);
+  }
+}
+
+// All tiles [t_begin, t_end) of one segment.
+template <int DT>
+__device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, uint64_t t_end,
+                                           uint32_t lane, Acc& acc) {
   constexpr int es = Et<DT>::es;
   constexpr int epc = 16 / es;
   constexpr int U = kDiffUnroll;
   const bool tol_mode = S.mode == ASMEVO_TOLERANCE;
   const bool strict = (S.flags & kSegStrict) != 0;
-  const uint64_t total = S.rows * S.row_chunks;
-  const uint64_t k0 = tile * (uint64_t)kTileChunks;
-  const uint8_t* a = reinterpret_cast<const uint8_t*>(S.a);
-  const uint8_t* b = reinterpret_cast<const uint8_t*>(S.b);
+  const bool vec = (S.flags & kSegVec) != 0;
+  const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
+  const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
 
-  if ((S.flags & (kSegVec | kSegTail)) == kSegVec && S.rows == 1 && k0 + kTileChunks <= total) {
-    // Fast path: a full tile of one contiguous segment.
-    const uint8_t* pa = a + (k0 + lane) * kChunk;
-    const uint8_t* pb = b + (k0 + lane) * kChunk;
-    u32x4 va[U], vb[U];
-#pragma unroll
-    for (int j = 0; j < U; ++j) {
-      va[j] = ld_nt(pa + j * kWave * kChunk);
-      vb[j] = ld_nt(pb + j * kWave * kChunk);
+  if (S.flags & kSegNarrow) {
+    // Short rows: tiles over the row-major chunk space, each lane finds its row.
+    const uint64_t total = S.rows * S.row_chunks;
+    for (uint64_t tile = t_begin; tile < t_end; ++tile) {
+      const uint64_t k0 = tile * (uint64_t)kTileChunks;
+#pragma unroll 1
+      for (int j = 0; j < U; ++j) {
+        const uint64_t k = k0 + (uint64_t)(j * kWave) + lane;
+        u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
+        uint32_t nb = 0;
+        uint64_t i0 = 0;
+        if (k < total) {
+          const uint64_t r = k / S.row_chunks;
+          const uint64_t c = k - r * S.row_chunks;
+          const uint64_t cb = c * kChunk;
+          const uint64_t rem = S.row_bytes - cb;
+          nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+          load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb, vec, va, vb);
+          i0 = r * S.cols + c * epc;
+        }
+        chunk<DT>(va, vb, i0, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
+      }
     }
-#pragma unroll
-    for (int j = 0; j < U; ++j)
-      chunk<DT>(va[j], vb[j], (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode, strict,
-                S.atol, S.rtol, acc);
     return;
   }
 
-  // General path: 2-D rows, partial chunks, misaligned operands, last tile.
-  const bool vec = (S.flags & kSegVec) != 0;
-  uint64_t r, c;
-  {
-    const uint64_t k = k0 + lane;
-    if (S.rows == 1) {
-      r = 0;
-      c = k;
-    } else {
-      r = k / S.row_chunks;
-      c = k - r * S.row_chunks;
-    }
-  }
-  u32x4 va[U], vb[U];
-  uint64_t i0[U];
-  uint32_t nv[U];
-#pragma unroll
-  for (int j = 0; j < U; ++j) {
-    const uint64_t kk = k0 + (uint64_t)(j * kWave) + lane;
-    va[j] = u32x4{0u, 0u, 0u, 0u};
-    vb[j] = u32x4{0u, 0u, 0u, 0u};
-    nv[j] = 0;
-    i0[j] = r * S.cols + c * epc;
-    if (kk < total) {
-      const uint64_t cb = c * kChunk;
-      const uint64_t rem = S.row_bytes - cb;
-      const uint32_t nbytes = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-      nv[j] = nbytes / es;
-      const uint8_t* pa = a + r * S.a_pitch + cb;
-      const uint8_t* pb = b + r * S.b_pitch + cb;
-      if (nbytes == kChunk && vec) {
-        va[j] = ld_nt(pa);
-        vb[j] = ld_nt(pb);
-      } else {
-        va[j] = load_elems<DT>(pa, nv[j]);
-        vb[j] = load_elems<DT>(pb, nv[j]);
-      }
-    }
-    c += kWave;
+  // Row-tiled: every tile lies inside one row.
+  const uint64_t tpr = S.tiles_per_row;
+  for (uint64_t tile = t_begin; tile < t_end; ++tile) {
+    uint64_t r = 0, kt = tile;
     if (S.rows > 1) {
-      while (c >= S.row_chunks) {
-        c -= S.row_chunks;
-        ++r;
+      r = (uint32_t)tile / (uint32_t)tpr;
+      kt = tile - r * tpr;
+    }
+    const uint8_t* pa = a0 + r * S.a_pitch;
+    const uint8_t* pb = b0 + r * S.b_pitch;
+    const uint64_t ibase = r * S.cols;
+    const uint64_t k0 = kt * (uint64_t)kTileChunks;
+    if (vec && k0 + kTileChunks <= S.full_chunks) {
+      // Fast path: every chunk of the tile is whole; issue all loads first.
+      const uint8_t* qa = pa + (k0 + lane) * kChunk;
+      const uint8_t* qb = pb + (k0 + lane) * kChunk;
+      u32x4 va[U], vb[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        va[j] = ld_nt(qa + j * kWave * kChunk);
+        vb[j] = ld_nt(qb + j * kWave * kChunk);
       }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        chunk<DT>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
+                  strict, S.atol, S.rtol, acc);
+      continue;
+    }
+    // Last tile of a row (or misaligned operands): per-chunk bounds.
+#pragma unroll 1
+    for (int j = 0; j < U; ++j) {
+      const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+      u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
+      uint32_t nb = 0;
+      if (c < S.row_chunks) {
+        const uint64_t cb = c * kChunk;
+        const uint64_t rem = S.row_bytes - cb;
+        nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+        load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
+      }
+      chunk<DT>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
     }
   }
-#pragma unroll
-  for (int j = 0; j < U; ++j)
-    chunk<DT>(va[j], vb[j], i0[j], nv[j], tol_mode, strict, S.atol, S.rtol, acc);
 }
 
 __device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
@@ -349,24 +368,25 @@ __global__ __launch_bounds__(kDiffBlock) void diff_kernel(const DiffSeg* __restr
   int s = s_lo;
   Acc acc;
   acc_reset(acc);
-  for (uint64_t t = lo; t < hi; ++t) {
-    while (s + 1 < n && segs[s + 1].tile_begin <= t) {
-      flush(acc, segs[s], results, lane);
-      ++s;
-    }
+  uint64_t t = lo;
+  while (t < hi) {
+    while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
     const DiffSeg S = segs[s];
-    const uint64_t tile = t - S.tile_begin;
+    const uint64_t seg_end = S.tile_begin + S.tile_count;
+    const uint64_t t_end = seg_end < hi ? seg_end : hi;
+    const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
     switch (S.dtype) {
-      case ASMEVO_F32: diff_tile<ASMEVO_F32>(S, tile, lane, acc); break;
-      case ASMEVO_BF16: diff_tile<ASMEVO_BF16>(S, tile, lane, acc); break;
-      case ASMEVO_F16: diff_tile<ASMEVO_F16>(S, tile, lane, acc); break;
-      case ASMEVO_FP8_E4M3: diff_tile<ASMEVO_FP8_E4M3>(S, tile, lane, acc); break;
-      case ASMEVO_I32: diff_tile<ASMEVO_I32>(S, tile, lane, acc); break;
-      case ASMEVO_I64: diff_tile<ASMEVO_I64>(S, tile, lane, acc); break;
-      default: diff_tile<ASMEVO_U8>(S, tile, lane, acc); break;
+      case ASMEVO_F32: diff_range<ASMEVO_F32>(S, b, e, lane, acc); break;
+      case ASMEVO_BF16: diff_range<ASMEVO_BF16>(S, b, e, lane, acc); break;
+      case ASMEVO_F16: diff_range<ASMEVO_F16>(S, b, e, lane, acc); break;
+      case ASMEVO_FP8_E4M3: diff_range<ASMEVO_FP8_E4M3>(S, b, e, lane, acc); break;
+      case ASMEVO_I32: diff_range<ASMEVO_I32>(S, b, e, lane, acc); break;
+      case ASMEVO_I64: diff_range<ASMEVO_I64>(S, b, e, lane, acc); break;
+      default: diff_range<ASMEVO_U8>(S, b, e, lane, acc); break;
     }
+    flush(acc, S, results, lane);
+    t = t_end;
   }
-  flush(acc, segs[s], results, lane);
 }
 
 }  // namespace

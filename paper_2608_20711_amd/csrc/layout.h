@@ -9,16 +9,19 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kChunk = 16;         // bytes per lane per load (dwordx4)
 
 // ---------------------------------------------------------------- diff
-constexpr int kDiffUnroll = 8;                       // chunks per lane per tile
-constexpr int kTileChunks = kWave * kDiffUnroll;     // 512 chunks = 8 KiB per side
+constexpr int kDiffUnroll = 4;                       // chunks per lane per tile
+constexpr int kTileChunks = kWave * kDiffUnroll;     // 256 chunks = 4 KiB per operand
 constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
 
 enum : uint32_t {
   kSegVec = 1u,       // a, b and both row pitches are 16-byte aligned
-  kSegTail = 2u,      // row bytes not a multiple of 16: last chunk of a row is partial
   kSegStrict = 4u,    // TOLERANCE with the strict NaN policy
+  kSegNarrow = 8u,    // short 2-D rows: tiles run over the flattened chunk space
 };
 
+// A segment is either "row-tiled" (every tile lies inside one row: contiguous
+// segments are one long row) or "narrow" (rows shorter than half a tile; tiles
+// run over the row-major chunk space and each lane finds its own row).
 struct DiffSeg {                // 128 bytes
   uint64_t a, b;                // element (0,0) of candidate / reference
   uint64_t a_pitch, b_pitch;    // bytes between row starts
@@ -26,11 +29,12 @@ struct DiffSeg {                // 128 bytes
   uint64_t cols;                // logical elements per (possibly flattened) row
   uint64_t row_bytes;           // cols * esize
   uint64_t row_chunks;          // ceil(row_bytes / 16)
+  uint64_t full_chunks;         // row_bytes / 16
   uint64_t tile_begin;          // first tile of this segment in the global tile space
   uint64_t tile_count;
   double atol, rtol;
   uint32_t dtype, mode, flags, esize;
-  uint32_t result_index, pad0, pad1, pad2;
+  uint32_t result_index, tiles_per_row;
 };
 static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
 
