@@ -30,6 +30,23 @@ HBM_PEAK_GBPS = 8000.0
 CPU_THREADS = 16
 
 
+def pmc_traffic():
+    """HBM bytes per diff launch from the committed rocprofv3 counter summary,
+    if the diff kernel's sources are still the ones that were profiled."""
+    import hashlib
+    summary = os.path.join(ROOT, "profiles", "diff_kernel_sweep_pmc.md")
+    try:
+        line = next(l for l in open(summary) if l.strip().startswith("PMC_TRAFFIC "))
+        rec = json.loads(line.strip()[len("PMC_TRAFFIC "):])
+    except (OSError, StopIteration, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in ("diff.hip", "layout.h", "device_math.h"):
+        with open(os.path.join(ROOT, "paper_2608_20711_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return rec["bytes_per_launch"] if h.hexdigest() == rec["source_sha256"] else None
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -41,6 +58,10 @@ def parse():
     p.add_argument("--cpu-sample-bytes", type=float, default=1.5 * 2 ** 30,
                    help="logical bytes per side of the oracle's sample")
     p.add_argument("--workgroups", type=int, default=0)
+    p.add_argument("--read-probe", type=int, default=-1, metavar="GIB",
+                   help="after the timed steps, run the two-stream HBM read probe over GIB per "
+                        "side and report it as the measured read ceiling (-1: the workload's "
+                        "own bytes per side, 0: skip)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="first copy BYTES device-to-device with torch (a plain copy kernel of known "
                         "size, to scale HBM traffic counters)")
@@ -173,14 +194,35 @@ def main():
         "fill_GBps": round(data_bytes / (statistics.median(fill_ms) * 1e-3) / 1e9, 1),
         "ref_fill_ms": round(ref_fill_ms, 3),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": pmc_traffic() if args.workload == "sweep" and not args.small else None,
                      "kernel": "diff_kernel (event span also holds the descriptor upload and result init)"},
         "total_mismatches": int(sum(r["mismatches"] for r in results)),
         "total_bitwise": int(sum(r["bitwise_mismatches"] for r in results)),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, st, results, args.cpu_sample_bytes)
+    if args.read_probe:
+        del st
+        torch.cuda.empty_cache()
+        gib = args.read_probe if args.read_probe > 0 else max(1, w.arena_bytes >> 30)
+        out["read_probe"] = read_probe(gib)
+        if "GBps" in out["read_probe"]:
+            out["pct_of_read_probe"] = round(100 * value / out["read_probe"]["GBps"], 2)
     print(json.dumps(out), flush=True)
+
+
+def read_probe(gib: int):
+    """Runs the in-tree read-ceiling probe (built with the library) as a child process."""
+    import subprocess
+    exe = os.path.join(ROOT, "read_probe")
+    if not os.path.exists(exe):
+        return {"error": "read_probe not built"}
+    p = subprocess.run([exe, str(gib)], capture_output=True, text=True, timeout=300)
+    try:
+        return json.loads(p.stdout.strip().splitlines()[-1])
+    except (ValueError, IndexError):
+        return {"error": (p.stdout + p.stderr)[-300:]}
 
 
 if __name__ == "__main__":

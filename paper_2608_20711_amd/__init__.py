@@ -14,7 +14,8 @@ import os
 from typing import Optional, Sequence
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libasmevo.so")
+# ASMEVO_LIBRARY may point at another build of the same library (tuning runs)
+LIB_PATH = os.environ.get("ASMEVO_LIBRARY") or os.path.join(PKG, "libasmevo.so")
 
 # codes of include/asmevo.h
 OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, -1, -2, -3, -4

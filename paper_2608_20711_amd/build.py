@@ -24,6 +24,10 @@ FLAGS = [
 ]
 
 
+PROBE_SRC = os.path.join(ROOT, "read_probe.hip")
+PROBE_EXE = os.path.join(ROOT, "read_probe")
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
@@ -39,5 +43,18 @@ def build(verbose: bool = False, extra=()) -> str:
     return LIB
 
 
+def build_probe(verbose: bool = False) -> str:
+    """Compiles the HBM read-ceiling probe that bench.py reports beside the diff."""
+    tmp = PROBE_EXE + ".tmp"
+    flags = [f for f in FLAGS if f not in ("-shared", "-fPIC")]
+    cmd = [HIPCC, *flags, PROBE_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, PROBE_EXE)
+    return PROBE_EXE
+
+
 if __name__ == "__main__":
     build(verbose=True, extra=sys.argv[1:])
+    build_probe(verbose=True)

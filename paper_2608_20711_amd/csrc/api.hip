@@ -318,7 +318,7 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
   int wg = workgroups;
-  if (wg == 0) wg = device_cus() * 4;          // 16 waves per CU
+  if (wg == 0) wg = device_cus() * diff_blocks_per_cu();   // one resident wave set, persistent
   HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(workspace), n, tiles, results, wg, s));
   return ASMEVO_OK;
 }

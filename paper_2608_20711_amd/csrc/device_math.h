@@ -14,6 +14,20 @@
 
 namespace asmevo {
 
+// Addresses arrive as integers in descriptor tables, so the compiler cannot
+// infer that they point to global memory; these casts make the accesses
+// global_load / global_store (not flat accesses, which are also checked
+// against LDS and scratch).
+#define AS_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ AS_GLOBAL T* gptr_mut(uint64_t addr) {
+  return (AS_GLOBAL T*)(uintptr_t)addr;
+}
+template <typename T>
+__device__ __forceinline__ const AS_GLOBAL T* gptr(const void* p) {
+  return (const AS_GLOBAL T*)(uintptr_t)p;
+}
+
 // ---------------------------------------------------------------------------
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).  One call turns a
 // 128-bit counter and 64-bit key into four 32-bit words.

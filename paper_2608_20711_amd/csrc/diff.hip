@@ -165,11 +165,11 @@ __device__ __forceinline__ u32x4 load_elems(const uint8_t* p, uint32_t nv) {
 #pragma unroll
   for (int e = 0; e < epc; ++e) {
     if ((uint32_t)e < nv) {
-      if constexpr (es == 1) w[e >> 2] |= (uint32_t)p[e] << (8 * (e & 3));
-      else if constexpr (es == 2) w[e >> 1] |= (uint32_t)reinterpret_cast<const uint16_t*>(p)[e] << (16 * (e & 1));
-      else if constexpr (es == 4) w[e] = reinterpret_cast<const uint32_t*>(p)[e];
+      if constexpr (es == 1) w[e >> 2] |= (uint32_t)gptr<uint8_t>(p)[e] << (8 * (e & 3));
+      else if constexpr (es == 2) w[e >> 1] |= (uint32_t)gptr<uint16_t>(p)[e] << (16 * (e & 1));
+      else if constexpr (es == 4) w[e] = gptr<uint32_t>(p)[e];
       else {
-        const uint64_t raw = reinterpret_cast<const uint64_t*>(p)[e];
+        const uint64_t raw = gptr<uint64_t>(p)[e];
         w[2 * e] = (uint32_t)raw;
         w[2 * e + 1] = (uint32_t)(raw >> 32);
       }
@@ -179,7 +179,7 @@ __device__ __forceinline__ u32x4 load_elems(const uint8_t* p, uint32_t nv) {
 }
 
 __device__ __forceinline__ u32x4 ld_nt(const uint8_t* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return __builtin_nontemporal_load(gptr<u32x4>(p));
 }
 
 // Chunk pair of a row whose bytes [c*16, c*16 + nbytes) are valid: a vector
@@ -238,7 +238,51 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
 
   // Row-tiled: every tile lies inside one row.
   const uint64_t tpr = S.tiles_per_row;
-  for (uint64_t tile = t_begin; tile < t_end; ++tile) {
+  uint64_t tile = t_begin;
+#if ASMEVO_DIFF_PIPELINE
+  if (S.rows == 1 && vec) {
+    // Contiguous segment: its whole tiles run as a software pipeline -- the
+    // loads of tile t+1 are in flight while tile t is checked.
+    const uint64_t whole = S.full_chunks / kTileChunks;
+    const uint64_t t_fast = t_end < whole ? t_end : whole;
+    if (tile < t_fast) {
+      const uint8_t* qa = a0 + (uint64_t)lane * kChunk;
+      const uint8_t* qb = b0 + (uint64_t)lane * kChunk;
+      u32x4 va[U], vb[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        va[j] = ld_nt(qa + (tile * kTileChunks + j * kWave) * kChunk);
+        vb[j] = ld_nt(qb + (tile * kTileChunks + j * kWave) * kChunk);
+      }
+      for (; tile < t_fast; ++tile) {
+        u32x4 na[U], nb[U];
+        if (tile + 1 < t_fast) {
+#pragma unroll
+          for (int j = 0; j < U; ++j) {
+            na[j] = ld_nt(qa + ((tile + 1) * kTileChunks + j * kWave) * kChunk);
+            nb[j] = ld_nt(qb + ((tile + 1) * kTileChunks + j * kWave) * kChunk);
+          }
+        }
+        u32x4 x = va[0] ^ vb[0];
+#pragma unroll
+        for (int j = 1; j < U; ++j) x |= va[j] ^ vb[j];
+        if (((x.x | x.y | x.z | x.w) != 0u) || strict) {
+          const uint64_t k0 = tile * (uint64_t)kTileChunks;
+#pragma unroll
+          for (int j = 0; j < U; ++j)
+            chunk<DT>(va[j], vb[j], (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode, strict,
+                      S.atol, S.rtol, acc);
+        }
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          va[j] = na[j];
+          vb[j] = nb[j];
+        }
+      }
+    }
+  }
+#endif
+  for (; tile < t_end; ++tile) {
     uint64_t r = 0, kt = tile;
     if (S.rows > 1) {
       r = (uint32_t)tile / (uint32_t)tpr;
@@ -249,7 +293,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
     const uint64_t ibase = r * S.cols;
     const uint64_t k0 = kt * (uint64_t)kTileChunks;
     if (vec && k0 + kTileChunks <= S.full_chunks) {
-      // Fast path: every chunk of the tile is whole; issue all loads first.
+      // Whole tile: issue all loads first, then one combined check.
       const uint8_t* qa = pa + (k0 + lane) * kChunk;
       const uint8_t* qb = pb + (k0 + lane) * kChunk;
       u32x4 va[U], vb[U];
@@ -258,10 +302,15 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
         va[j] = ld_nt(qa + j * kWave * kChunk);
         vb[j] = ld_nt(qb + j * kWave * kChunk);
       }
+      u32x4 x = va[0] ^ vb[0];
 #pragma unroll
-      for (int j = 0; j < U; ++j)
-        chunk<DT>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
-                  strict, S.atol, S.rtol, acc);
+      for (int j = 1; j < U; ++j) x |= va[j] ^ vb[j];
+      if (((x.x | x.y | x.z | x.w) != 0u) || strict) {
+#pragma unroll
+        for (int j = 0; j < U; ++j)
+          chunk<DT>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
+                    strict, S.atol, S.rtol, acc);
+      }
       continue;
     }
     // Last tile of a row (or misaligned operands): per-chunk bounds.
@@ -349,7 +398,9 @@ __global__ void diff_init_kernel(asmevo_segment_result* results, int n) {
   results[t] = r;
 }
 
-__global__ __launch_bounds__(kDiffBlock) void diff_kernel(const DiffSeg* __restrict__ segs, int n,
+
+__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(ASMEVO_DIFF_WAVES_PER_EU)))
+void diff_kernel(const DiffSeg* __restrict__ segs, int n,
                                                           uint64_t total_tiles,
                                                           asmevo_segment_result* results) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
@@ -391,14 +442,21 @@ __global__ __launch_bounds__(kDiffBlock) void diff_kernel(const DiffSeg* __restr
 
 }  // namespace
 
+int diff_blocks_per_cu() {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel, kDiffBlock, 0) != hipSuccess ||
+      blocks <= 0)
+    blocks = 4;
+  return blocks;
+}
+
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(diff_init_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, results, n);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || total_tiles == 0) return e;
-  const uint64_t waves_needed = total_tiles;
-  const uint64_t max_wg = (waves_needed + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
+  const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
   const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
   hipLaunchKernelGGL(diff_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n, total_tiles,
                      results);

@@ -181,32 +181,59 @@ __device__ __forceinline__ void put_elem(uint32_t w[4], uint32_t m, uint64_t v) 
 }
 
 // 16 data bytes holding exactly 16/es whole elements starting at logical
-// index i0 of one row.
+// index i0 of one row.  When i0 is a multiple of 4 the chunk is made of whole
+// generator blocks: each VALUE and SELECT block is drawn once for its four
+// elements.
 template <int DT>
 __device__ __forceinline__ void data_chunk(const FillAlloc& A, const FillRule* rules, uint64_t i0,
                                            uint64_t seed, uint32_t w[4]) {
   constexpr int es = Elem<DT>::es;
   constexpr int epc = 16 / es;
   w[0] = w[1] = w[2] = w[3] = 0;
-  if (es <= 4 && A.dist == ASMEVO_DIST_NORMAL && (i0 & 3u) == 0) {
-    // whole generator blocks: one Philox call and two Box-Muller pairs per 4 elements
+  if (es <= 4 && (i0 & 3u) == 0 &&
+      (A.dist == ASMEVO_DIST_NORMAL || A.dist == ASMEVO_DIST_UNIFORM_INT)) {
 #pragma unroll 1
     for (uint32_t blk = 0; blk < (uint32_t)(epc / 4); ++blk) {
-      const U4 X = stream(seed, A.alloc_id, kValue, 0, 0, (i0 >> 2) + blk);
+      const uint64_t j = (i0 >> 2) + blk;
+      const U4 X = stream(seed, A.alloc_id, kValue, 0, 0, j);
+      uint64_t base[4];
+      if (A.dist == ASMEVO_DIST_NORMAL) {
 #pragma unroll 1
-      for (uint32_t h = 0; h < 2; ++h) {
-        double z0, z1;
-        box_muller(h ? X.z : X.x, h ? X.w : X.y, z0, z1);
+        for (uint32_t h = 0; h < 2; ++h) {
+          double z0, z1;
+          box_muller(h ? X.z : X.x, h ? X.w : X.y, z0, z1);
+          const double v0 = A.p0 + A.p1 * z0;
+          const double v1 = A.p0 + A.p1 * z1;
+          const uint64_t e0 = encode_f32(DT, (float)v0, A.saturate != 0);
+          const uint64_t e1 = encode_f32(DT, (float)v1, A.saturate != 0);
+          base[0] = h ? base[0] : e0;
+          base[1] = h ? base[1] : e1;
+          base[2] = h ? e0 : base[2];
+          base[3] = h ? e1 : base[3];
+        }
+      } else {
 #pragma unroll
-        for (uint32_t t = 0; t < 2; ++t) {
-          const uint32_t m = blk * 4 + h * 2 + t;
-          const double scaled = A.p1 * (t ? z1 : z0);
-          const double val = A.p0 + scaled;
-          uint64_t bits = encode_f32(DT, (float)val, A.saturate != 0);
-          if (A.rule_count) bits = apply_rules(A, rules, bits, seed, i0 + m);
-          put_elem<es>(w, m, bits);
+        for (int t = 0; t < 4; ++t) base[t] = base_from_block(A, X, 4 * j + t, seed);
+      }
+      uint64_t val[4] = {base[0], base[1], base[2], base[3]};
+      for (uint32_t r = 0; r < A.rule_count; ++r) {
+        const FillRule R = rules[A.rule_begin + r];
+        const U4 S = stream(seed, A.alloc_id, kSelect, R.ordinal, R.vsel, j);
+        uint32_t sel = ((uint64_t)S.x < R.threshold ? 1u : 0u) | ((uint64_t)S.y < R.threshold ? 2u : 0u) |
+                       ((uint64_t)S.z < R.threshold ? 4u : 0u) | ((uint64_t)S.w < R.threshold ? 8u : 0u);
+        while (sel) {                       // rare: the selected elements of this block
+          const uint32_t t = (uint32_t)__builtin_ctz(sel);
+          sel &= sel - 1u;
+          const uint64_t b = t == 0 ? base[0] : t == 1 ? base[1] : t == 2 ? base[2] : base[3];
+          const uint64_t v = apply_injection(A, R.kind, R.vsel, R.arg, R.atol, R.rtol, b, seed, 4 * j + t);
+          val[0] = t == 0 ? v : val[0];
+          val[1] = t == 1 ? v : val[1];
+          val[2] = t == 2 ? v : val[2];
+          val[3] = t == 3 ? v : val[3];
         }
       }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) put_elem<es>(w, blk * 4 + t, val[t]);
     }
   } else {
 #pragma unroll 1
@@ -300,12 +327,12 @@ __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillRul
     }
   }
   if (!done) general_chunk(A, rules, o, seed, w);
-  uint8_t* dst = reinterpret_cast<uint8_t*>(A.base) + o;
   if (o + 16 <= tot) {
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    u32x4 v = {w[0], w[1], w[2], w[3]};
-    *reinterpret_cast<u32x4*>(dst) = v;
+    const u32x4 v = {w[0], w[1], w[2], w[3]};
+    *gptr_mut<u32x4>(A.base + o) = v;
   } else {
+    AS_GLOBAL uint8_t* dst = gptr_mut<uint8_t>(A.base + o);
     for (uint32_t b = 0; o + b < tot; ++b) dst[b] = (uint8_t)(w[b >> 2] >> (8u * (b & 3u)));
   }
 }
@@ -345,10 +372,9 @@ __global__ void inject_kernel(const FillAlloc* __restrict__ allocs,
   if (t >= n_pts) return;
   const PointEntry P = pts[t];
   const FillAlloc A = allocs[P.alloc];
-  uint8_t* base = reinterpret_cast<uint8_t*>(A.base);
   if (P.kind == ASMEVO_INJ_GUARD_WRITE_LO || P.kind == ASMEVO_INJ_GUARD_WRITE_HI) {
     const uint32_t side = P.kind == ASMEVO_INJ_GUARD_WRITE_HI;
-    uint8_t* g = side ? base + A.guard_lo + A.data_bytes : base;
+    AS_GLOBAL uint8_t* g = gptr_mut<uint8_t>(side ? A.base + A.guard_lo + A.data_bytes : A.base);
     for (uint32_t b = 0; b < P.arg; ++b) {
       const uint64_t p = (uint64_t)P.index + b;
       g[p] = (uint8_t)~canary_byte(A.alloc_id, side, p, seed);
@@ -359,12 +385,12 @@ __global__ void inject_kernel(const FillAlloc* __restrict__ allocs,
   const uint64_t v = apply_injection(A, P.kind, P.vsel, P.arg, P.atol, P.rtol,
                                      base_element(A, i, seed), seed, i);
   const uint64_t r = i / A.cols, c = i - r * A.cols;
-  uint8_t* dst = base + A.guard_lo + (r * A.stride + c) * A.esize;
+  const uint64_t dst = A.base + A.guard_lo + (r * A.stride + c) * A.esize;
   switch (A.esize) {
-    case 1: *dst = (uint8_t)v; break;
-    case 2: *reinterpret_cast<uint16_t*>(dst) = (uint16_t)v; break;
-    case 4: *reinterpret_cast<uint32_t*>(dst) = (uint32_t)v; break;
-    default: *reinterpret_cast<uint64_t*>(dst) = v; break;
+    case 1: *gptr_mut<uint8_t>(dst) = (uint8_t)v; break;
+    case 2: *gptr_mut<uint16_t>(dst) = (uint16_t)v; break;
+    case 4: *gptr_mut<uint32_t>(dst) = (uint32_t)v; break;
+    default: *gptr_mut<uint64_t>(dst) = v; break;
   }
 }
 

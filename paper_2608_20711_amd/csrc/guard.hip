@@ -41,16 +41,17 @@ __global__ __launch_bounds__(256) void guard_kernel(const GuardRegion* __restric
     const uint64_t left = R.bytes - p0;
     const uint32_t nb = left < (uint64_t)kChunk ? (uint32_t)left : (uint32_t)kChunk;
     const U4 C = stream(seed, R.alloc_id, kCanary, R.side, 0, p0 >> 4);
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(R.addr) + p0;
+    const uint64_t src = R.addr + p0;
     uint32_t mask = 0;
-    if (nb == (uint32_t)kChunk && (reinterpret_cast<uintptr_t>(src) & 15u) == 0) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+    if (nb == (uint32_t)kChunk && (src & 15u) == 0) {
+      const u32x4 v = *gptr_mut<u32x4>(src);
       const uint32_t x[4] = {v.x ^ C.x, v.y ^ C.y, v.z ^ C.z, v.w ^ C.w};
 #pragma unroll
       for (int k = 0; k < 16; ++k) mask |= ((x[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? (1u << k) : 0u;
     } else {
+      const AS_GLOBAL uint8_t* bytes = gptr_mut<uint8_t>(src);
       for (uint32_t k = 0; k < nb; ++k)
-        mask |= (src[k] != byte_of(C, k)) ? (1u << k) : 0u;
+        mask |= (bytes[k] != byte_of(C, k)) ? (1u << k) : 0u;
     }
     if (mask) {
       asmevo_guard_result* res = results + R.result_index;

@@ -13,6 +13,8 @@ hipError_t launch_fill(const FillAlloc* allocs, int n, const FillRule* rules, ui
 hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_pts, uint64_t seed,
                          hipStream_t stream);
 
+// Resident diff workgroups per compute unit (from the occupancy calculator).
+int diff_blocks_per_cu();
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream);
 

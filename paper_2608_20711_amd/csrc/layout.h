@@ -9,7 +9,16 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kChunk = 16;         // bytes per lane per load (dwordx4)
 
 // ---------------------------------------------------------------- diff
-constexpr int kDiffUnroll = 4;                       // chunks per lane per tile
+#ifndef ASMEVO_DIFF_UNROLL
+#define ASMEVO_DIFF_UNROLL 4
+#endif
+constexpr int kDiffUnroll = ASMEVO_DIFF_UNROLL;      // chunks per lane per tile
+#ifndef ASMEVO_DIFF_PIPELINE                         // contiguous segments double-buffer tiles
+#define ASMEVO_DIFF_PIPELINE 0
+#endif
+#ifndef ASMEVO_DIFF_WAVES_PER_EU                     // occupancy target of the diff kernel
+#define ASMEVO_DIFF_WAVES_PER_EU 4
+#endif
 constexpr int kTileChunks = kWave * kDiffUnroll;     // 256 chunks = 4 KiB per operand
 constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
 

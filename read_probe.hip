@@ -1,0 +1,96 @@
+// read_probe.hip -- measured HBM read ceiling for the segmented diff.
+//
+// Streams two buffers the way the diff kernel reads a candidate and a
+// reference state (16-byte non-temporal loads, 64 lanes x U chunks per tile,
+// each wave walking a contiguous range of tiles) and folds them with XOR, so
+// the only work is the read.  Prints one JSON line with the median and best
+// GB/s over several launches.  Built by the package build step; bench.py runs
+// it and reports the result beside the diff kernel's bandwidth.
+//
+// usage: read_probe [GiB per side (default 32)] [reps (default 7)]
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define CHECK(x)                                                                      \
+  do {                                                                                \
+    hipError_t e_ = (x);                                                              \
+    if (e_ != hipSuccess) {                                                           \
+      std::printf("{\"error\": \"%s at line %d\"}\n", hipGetErrorString(e_), __LINE__); \
+      std::exit(1);                                                                   \
+    }                                                                                 \
+  } while (0)
+
+constexpr int kU = 4;          // chunks per lane per tile, as in the diff kernel
+constexpr int kWavesPerBlock = 4;
+
+__global__ __launch_bounds__(kWavesPerBlock * 64) void read_two(const uint8_t* a, const uint8_t* b,
+                                                               uint64_t n_tiles, uint32_t* out) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t wave = (uint64_t)blockIdx.x * kWavesPerBlock +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const uint64_t nw = (uint64_t)gridDim.x * kWavesPerBlock;
+  const uint64_t lo = n_tiles * wave / nw, hi = n_tiles * (wave + 1) / nw;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (uint64_t t = lo; t < hi; ++t) {
+    const uint8_t* pa = a + (t * kU * 64 + lane) * 16;
+    const uint8_t* pb = b + (t * kU * 64 + lane) * 16;
+    u32x4 va[kU], vb[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      va[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(pa + j * 1024));
+      vb[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(pb + j * 1024));
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) acc ^= va[j] ^ vb[j];
+  }
+  out[(uint64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc.x | acc.y | acc.z | acc.w;
+}
+
+int main(int argc, char** argv) {
+  const uint64_t per_side = (argc > 1 ? std::strtoull(argv[1], nullptr, 10) : 32ull) << 30;
+  const int reps = argc > 2 ? std::atoi(argv[2]) : 7;
+  int cus = 0;
+  CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
+  const int blocks = cus * 4;
+  const uint64_t tile_bytes = (uint64_t)kU * 64 * 16;
+  const uint64_t n_tiles = per_side / tile_bytes;         // every tile lies inside both buffers
+  uint8_t *a = nullptr, *b = nullptr;
+  uint32_t* out = nullptr;
+  CHECK(hipMalloc(&a, per_side));
+  CHECK(hipMalloc(&b, per_side));
+  CHECK(hipMalloc(&out, (size_t)blocks * kWavesPerBlock * 64 * sizeof(uint32_t)));
+  CHECK(hipMemset(a, 0x5A, per_side));
+  CHECK(hipMemset(b, 0x5A, per_side));
+  CHECK(hipDeviceSynchronize());
+  hipEvent_t e0, e1;
+  CHECK(hipEventCreate(&e0));
+  CHECK(hipEventCreate(&e1));
+  std::vector<float> ms;
+  for (int r = 0; r < reps + 1; ++r) {
+    CHECK(hipEventRecord(e0));
+    hipLaunchKernelGGL(read_two, dim3(blocks), dim3(kWavesPerBlock * 64), 0, 0, a, b, n_tiles, out);
+    CHECK(hipGetLastError());
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    float t = 0.f;
+    CHECK(hipEventElapsedTime(&t, e0, e1));
+    if (r > 0) ms.push_back(t);                             // first launch is a warmup
+  }
+  std::sort(ms.begin(), ms.end());
+  const double bytes = 2.0 * (double)n_tiles * (double)tile_bytes;
+  const double med = ms[ms.size() / 2];
+  std::printf("{\"GBps\": %.1f, \"best_GBps\": %.1f, \"median_ms\": %.4f, \"bytes\": %.0f, "
+              "\"config\": \"2 x %llu GiB, nt dwordx4, U=%d, %d workgroups x %d waves\"}\n",
+              bytes / (med * 1e-3) / 1e9, bytes / (ms[0] * 1e-3) / 1e9, med, bytes,
+              (unsigned long long)(per_side >> 30), kU, blocks, kWavesPerBlock);
+  CHECK(hipFree(a));
+  CHECK(hipFree(b));
+  CHECK(hipFree(out));
+  return 0;
+}
