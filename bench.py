@@ -62,6 +62,10 @@ def parse():
                    help="after the timed steps, run the two-stream HBM read probe over GIB per "
                         "side and report it as the measured read ceiling (-1: the workload's "
                         "own bytes per side, 0: skip)")
+    p.add_argument("--flush-mib", type=int, default=-1,
+                   help="MiB written to a scratch buffer after each candidate fill, outside the timed "
+                        "span, so the diff reads HBM rather than the 256 MB Infinity Cache (-1: 1024 "
+                        "when a side is under 4 GiB, else 0)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="first copy BYTES device-to-device with torch (a plain copy kernel of known "
                         "size, to scale HBM traffic counters)")
@@ -149,8 +153,13 @@ def main():
     ref_fill_ms = e0.elapsed_time(e1)
     print(f"# reference fill {ref_fill_ms:.1f} ms", file=sys.stderr, flush=True)
 
+    flush_mib = args.flush_mib if args.flush_mib >= 0 else (1024 if w.arena_bytes < (4 << 30) else 0)
+    scratch = torch.empty(flush_mib << 20, dtype=torch.uint8, device="cuda:0") if flush_mib else None
+
     def step(variant, ev):
         st.fill("cand", variant, stream)
+        if scratch is not None:
+            scratch.fill_(variant & 0xFF)
         ev[0].record(stream)
         st.diff(stream, args.workgroups)
         ev[1].record(stream)
@@ -185,7 +194,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32-xor/f64",
         "data": "synthetic (seeded Philox fills; no datasets)",
-        "config": {"workload": w.description, "buffers": len(w.allocs),
+        "config": {"workload": w.description, "buffers": len(w.allocs), "cache_flush_mib": flush_mib,
                    "bytes_per_side": data_bytes, "logical_bytes_per_side": logical,
                    "compared_bytes": compared, "candidates_timed": args.steps},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),

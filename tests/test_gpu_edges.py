@@ -178,13 +178,17 @@ def test_zero_segments_and_argument_errors():
 
 # ------------------------------------------------------------------ fills
 def _fill_parity(w, variants=(0, 1, 2)):
+    """Fill parity for each variant, and guard-check parity on each fill."""
     from paper_2608_20711_amd.state import DeviceState
     st = DeviceState(w)
     P = oracle.Prepared(w)
     for v in variants:
         st.fill("cand", v)
+        st.guard()
         torch.cuda.synchronize()
-        assert_fill_equal(w, st.arena_host("cand"), P.fill_arena(v, THREADS), f"{w.name} variant {v}")
+        cand = P.fill_arena(v, THREADS)
+        assert_fill_equal(w, st.arena_host("cand"), cand, f"{w.name} variant {v}")
+        assert_results_equal(st.guard_results(), oracle.guard_workload(w, cand), f"{w.name} guards {v}")
     return st
 
 
@@ -245,4 +249,7 @@ def test_fill_geometry_distributions_and_injections():
         Injection(11, "set_nan", index=3),
     ]
     w = Workload("geometry", "", 0xFEEDFACE, allocs, inj, [])
-    _fill_parity(w, variants=(0, 1, 7, 65535))
+    st = _fill_parity(w, variants=(0, 1, 7, 65535))
+    g = st.guard_results()
+    assert g[0]["bad_lo"] == 3 and g[0]["first_bad_lo"] == 7 and g[0]["bad_hi"] == 40
+    assert g[9]["bad_hi"] == 8 and g[9]["first_bad_hi"] == 0
