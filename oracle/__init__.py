@@ -79,6 +79,14 @@ class RefSegResult(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class RefCosResult(ctypes.Structure):
+    _fields_ = [("sum_ab", ctypes.c_double), ("sum_aa", ctypes.c_double), ("sum_bb", ctypes.c_double),
+                ("cosine", ctypes.c_double), ("pairs", ctypes.c_uint64), ("blocks", ctypes.c_uint64)]
+
+    def as_dict(self) -> Dict:
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 class RefGuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
                 ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
@@ -116,6 +124,9 @@ def lib() -> ctypes.CDLL:
                                      ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
                                      ctypes.c_int64, vp]
         L.ref_diff_segment.argtypes = [P(RefSeg), vp, vp, P(RefSegResult)]
+        L.ref_cosine_segment.argtypes = [P(RefSeg), vp, vp, P(RefCosResult)]
+        L.ref_pairwise_tree.argtypes = [vp, ctypes.c_int64]
+        L.ref_pairwise_tree.restype = ctypes.c_double
         L.ref_guard_check.argtypes = [ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_int64,
                                       vp, ctypes.c_int64, P(RefGuardResult)]
         L.ref_decode_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, vp, vp]
@@ -273,6 +284,36 @@ def diff_segment(dtype: str, mode: str, nan_policy: str, rows: int, cols: int,
     if rc != 0:
         raise ValueError("oracle diff rejected the segment")
     return res.as_dict()
+
+
+def cosine_segment(dtype: str, rows: int, cols: int, stride_a: int, stride_b: int,
+                   a: np.ndarray, b: np.ndarray, a_off: int = 0, b_off: int = 0) -> Dict:
+    """Cosine term of Eq. 1 in the defined reduction order (see ref_oracle.h)."""
+    seg = RefSeg(DTYPE[dtype], MODE["bitwise"], 0, 0, rows, cols, stride_a, stride_b, 0.0, 0.0)
+    res = RefCosResult()
+    a = np.ascontiguousarray(a).view(np.uint8)
+    b = np.ascontiguousarray(b).view(np.uint8)
+    rc = lib().ref_cosine_segment(ctypes.byref(seg), _ptr(a) + a_off, _ptr(b) + b_off, ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle cosine rejected the segment")
+    return res.as_dict()
+
+
+def pairwise_tree(x: np.ndarray) -> float:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    return float(lib().ref_pairwise_tree(_ptr(x) if x.size else None, x.size))
+
+
+def cosine_workload(w, cand: np.ndarray, ref: np.ndarray, threads: int = 1) -> List[Dict]:
+    def one(c):
+        a = w.allocs[c.alloc]
+        off = w.data_offset(c.alloc)
+        return cosine_segment(a.dtype, a.rows, a.cols, a.stride, a.stride, cand, ref, off, off)
+    if threads <= 1:
+        return [one(c) for c in w.compares]
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(one, w.compares))
 
 
 def diff_workload(w, cand: np.ndarray, ref: np.ndarray, threads: int = 1) -> List[Dict]:

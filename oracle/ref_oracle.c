@@ -33,6 +33,7 @@
 #include "ref_oracle.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 /* ------------------------------------------------------------------------ */
@@ -557,6 +558,105 @@ int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref
         if (nonfinite) res->nonfinite_mismatches += 1;
       }
     }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Cosine term of Eq. 1: c = cos(K'(x), O(x)).  The products of two values   */
+/* of any of the float element types are exact in fp64, so every rounding    */
+/* below is an addition, taken in this defined order.                        */
+/* ------------------------------------------------------------------------ */
+
+/* Left-complete pairwise tree: P(x[0..n)) = x[0] for n = 1, otherwise
+ * P(x[0..h)) + P(x[h..n)) with h the largest power of two below n. */
+double ref_pairwise_tree(const double* x, int64_t n) {
+  if (n <= 0) return 0.0;
+  if (n == 1) return x[0];
+  int64_t h = 1;
+  while (h * 2 < n) h *= 2;
+  double left = ref_pairwise_tree(x, h);
+  double right = ref_pairwise_tree(x + h, n - h);
+  return left + right;
+}
+
+int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res) {
+  int es = ref_esize(seg->dtype);
+  if (es == 0) return -1;
+  res->sum_ab = 0.0;
+  res->sum_aa = 0.0;
+  res->sum_bb = 0.0;
+  res->cosine = NAN;
+  res->pairs = 0;
+  res->blocks = 0;
+  if (!is_float(seg->dtype)) return 0;       /* not defined for integer buffers */
+  int64_t rows = seg->rows, cols = seg->cols;
+  if (rows <= 0 || cols <= 0) {
+    rows = 0;
+  } else if (rows == 1 || (seg->stride_a == cols && seg->stride_b == cols)) {
+    cols = rows * cols;                       /* one contiguous row */
+    rows = 1;
+  }
+  int64_t per_block = 4096 / es;              /* elements of a 4096-byte block */
+  int64_t per_chunk = 16 / es;                /* elements of a 16-byte chunk */
+  int64_t blocks_per_row = rows ? (cols + per_block - 1) / per_block : 0;
+  int64_t nblocks = rows * blocks_per_row;
+  double* bab = (double*)malloc(sizeof(double) * (size_t)(nblocks ? nblocks : 1) * 3);
+  if (!bab) return -1;
+  double* baa = bab + nblocks;
+  double* bbb = baa + nblocks;
+  int64_t k = 0;
+  for (int64_t r = 0; r < rows; ++r) {
+    for (int64_t blk = 0; blk < blocks_per_row; ++blk, ++k) {
+      double lab[64], laa[64], lbb[64];
+      for (int L = 0; L < 64; ++L) lab[L] = laa[L] = lbb[L] = 0.0;
+      int64_t c0 = blk * per_block;
+      int64_t len = cols - c0 < per_block ? cols - c0 : per_block;
+      for (int64_t t = 0; t < len; ++t) {
+        int64_t c = c0 + t;
+        uint64_t ra = load_raw(a + (r * seg->stride_a + c) * es, es);
+        uint64_t rb = load_raw(b + (r * seg->stride_b + c) * es, es);
+        double A, B;
+        if (ref_decode(seg->dtype, ra, &A) != 0 || ref_decode(seg->dtype, rb, &B) != 0) continue;
+        int L = (int)((t / per_chunk) % 64);
+        lab[L] = lab[L] + A * B;
+        laa[L] = laa[L] + A * A;
+        lbb[L] = lbb[L] + B * B;
+        res->pairs += 1;
+      }
+      /* xor butterfly over the 64 lanes */
+      for (int m = 32; m >= 1; m /= 2) {
+        double nab[64], naa[64], nbb[64];
+        for (int L = 0; L < 64; ++L) {
+          nab[L] = lab[L] + lab[L ^ m];
+          naa[L] = laa[L] + laa[L ^ m];
+          nbb[L] = lbb[L] + lbb[L ^ m];
+        }
+        for (int L = 0; L < 64; ++L) {
+          lab[L] = nab[L];
+          laa[L] = naa[L];
+          lbb[L] = nbb[L];
+        }
+      }
+      bab[k] = lab[0];
+      baa[k] = laa[0];
+      bbb[k] = lbb[0];
+    }
+  }
+  res->blocks = (uint64_t)nblocks;
+  res->sum_ab = ref_pairwise_tree(bab, nblocks);
+  res->sum_aa = ref_pairwise_tree(baa, nblocks);
+  res->sum_bb = ref_pairwise_tree(bbb, nblocks);
+  free(bab);
+  if (res->sum_aa == 0.0 && res->sum_bb == 0.0) {
+    res->cosine = 1.0;                        /* both vectors are zero */
+  } else if (res->sum_aa == 0.0 || res->sum_bb == 0.0) {
+    res->cosine = 0.0;                        /* exactly one is zero */
+  } else {
+    double na = sqrt(res->sum_aa);
+    double nb = sqrt(res->sum_bb);
+    double den = na * nb;
+    res->cosine = res->sum_ab / den;
   }
   return 0;
 }

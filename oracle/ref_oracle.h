@@ -102,6 +102,20 @@ int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref
 int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t n_lo,
                     const uint8_t* hi, int64_t n_hi, ref_guard_result* res);
 
+/* Cosine term of Eq. 1 over one segment (float dtypes).  sum_* are fp64
+ * sums over the pairs with both values finite, in the defined order: rows
+ * (a segment contiguous in both operands is one row), 4096-byte blocks of a
+ * row, 64 lanes per block taking every 64th 16-byte chunk, an xor butterfly
+ * over the lanes, and a left-complete pairwise tree over the blocks. */
+typedef struct {
+  double sum_ab, sum_aa, sum_bb, cosine;
+  uint64_t pairs;        /* pairs with both values finite */
+  uint64_t blocks;
+} ref_cos_result;
+int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res);
+/* the left-complete pairwise tree alone (exposed for its pins) */
+double ref_pairwise_tree(const double* x, int64_t n);
+
 /* bulk loops over the scalar functions above (used by the pin tests) */
 void ref_decode_n(int32_t dtype, const uint64_t* raw, int64_t n, int32_t* cls, double* value);
 void ref_encode_f32_n(int32_t dtype, const float* x, int64_t n, int saturate, uint64_t* out);
