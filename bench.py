@@ -58,6 +58,9 @@ def parse():
     p.add_argument("--cpu-sample-bytes", type=float, default=1.5 * 2 ** 30,
                    help="logical bytes per side of the oracle's sample")
     p.add_argument("--workgroups", type=int, default=0)
+    p.add_argument("--cosine-steps", type=int, default=5,
+                   help="after the timed steps, time the diff + cosine pass (Eq. 1's c_x) this many "
+                        "times on the last candidate and report it beside the metric (0: skip)")
     p.add_argument("--read-probe", type=int, default=-1, metavar="GIB",
                    help="after the timed steps, run the two-stream HBM read probe over GIB per "
                         "side and report it as the measured read ceiling (-1: the workload's "
@@ -189,6 +192,29 @@ def main():
     diff_bytes = 2 * sum(w.allocs[c.alloc].n_elements * w.allocs[c.alloc].esize for c in w.compares)
     achieved = diff_bytes / (med_diff * 1e-3) / 1e9
     results = st.seg_results()
+    cosine = None
+    if args.cosine_steps > 0:
+        st.diff_cosine(stream)                      # sizes and allocates its workspace once
+        torch.cuda.synchronize()
+        cms = []
+        for _ in range(args.cosine_steps):
+            if scratch is not None:
+                scratch.fill_(0x5A)
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record(stream)
+            st.diff_cosine(stream)
+            c1.record(stream)
+            torch.cuda.synchronize()
+            cms.append(c0.elapsed_time(c1))
+        cos_res = st.cos_results()
+        seg_after = st.seg_results()
+        med_c = statistics.median(cms)
+        floats = [r for r, c in zip(cos_res, w.compares) if w.allocs[c.alloc].dtype in workloads.FLOAT_DTYPES]
+        cosine = {"ms_median": round(med_c, 4), "GBps": round(diff_bytes / (med_c * 1e-3) / 1e9, 2),
+                  "pct_of_hbm_peak": round(100 * diff_bytes / (med_c * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+                  "min_cosine": min((r["cosine"] for r in floats), default=None),
+                  "diff_results_identical": seg_after == results,
+                  "note": "one pass: diff + fp64 a*b, a*a, b*b per 4096-byte block, then the block tree"}
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 3),
@@ -206,6 +232,7 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": pmc_traffic() if args.workload == "sweep" and not args.small else None,
                      "kernel": "diff_kernel (event span also holds the descriptor upload and result init)"},
+        "diff_cosine": cosine,
         "total_mismatches": int(sum(r["mismatches"] for r in results)),
         "total_bitwise": int(sum(r["bitwise_mismatches"] for r in results)),
     }

@@ -221,6 +221,50 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
                                       void* workspace, size_t ws_bytes, void* stream,
                                       int32_t workgroups);
 
+/*
+ * Cosine term of Eq. 1 (section 3.2): c_x = cos(K'(x), O(x)) per buffer,
+ * over the element pairs with both values finite.  The products of two
+ * values of any float element type are exact in fp64, so only the additions
+ * round, and they follow one defined order, independent of launch geometry:
+ *   - rows: a segment whose operands are both contiguous (rows == 1, or
+ *     stride_a == stride_b == cols) is one row of rows*cols elements;
+ *     otherwise every row is separate;
+ *   - each row is cut into blocks of 4096 bytes (4096/esize elements, the
+ *     last block of a row shorter);
+ *   - in a block, element t belongs to lane (t / (16/esize)) mod 64; each lane
+ *     adds its products in increasing t, starting from +0.0;
+ *   - the 64 lane sums combine by an xor butterfly: for m = 32, 16, 8, 4, 2, 1
+ *     every lane adds the lane m apart; the block sum is lane 0's value;
+ *   - the blocks of the segment (row-major) combine by the left-complete
+ *     pairwise tree P(x[0..n)) = P(x[0..h)) + P(x[h..n)), h the largest power
+ *     of two below n, P of one value = that value, P of none = +0.0.
+ * cosine = sum_ab / (sqrt(sum_aa) * sqrt(sum_bb)), each operation rounded;
+ * 1.0 when both sums of squares are 0, 0.0 when exactly one is.  Integer and
+ * opaque buffers: sums 0, pairs 0, cosine NaN (not defined).
+ */
+typedef struct {
+  double sum_ab, sum_aa, sum_bb, cosine;
+  uint64_t pairs;    /* element pairs with both values finite */
+  uint64_t blocks;   /* 4096-byte blocks summed */
+} asmevo_cosine_result;
+
+/*
+ * asmevo_diff_cosine -- asmevo_diff_segments plus the cosine term of every
+ * float segment, from the same single pass over the operands (a second, small
+ * kernel folds the per-block sums).  `results` as for asmevo_diff_segments;
+ * `cos_results[0..n)` device memory.  The workspace must hold
+ * asmevo_diff_cosine_workspace_bytes(segs, n) bytes (it keeps 24 bytes per
+ * 4096-byte block).  Errors as for asmevo_diff_segments.
+ */
+asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
+                                 asmevo_segment_result* results,
+                                 asmevo_cosine_result* cos_results,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes asmevo_diff_cosine needs for these segments (0 if they are
+ * invalid). */
+size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n);
+
 /* Per-allocation guard result: counts of corrupted bytes and the lowest
  * corrupted byte offset within each guard (-1 if intact). */
 typedef struct {

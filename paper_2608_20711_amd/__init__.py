@@ -70,6 +70,11 @@ class SegmentResult(ctypes.Structure):
                 ("max_abs", ctypes.c_double), ("max_rel", ctypes.c_double)]
 
 
+class CosineResult(ctypes.Structure):
+    _fields_ = [("sum_ab", ctypes.c_double), ("sum_aa", ctypes.c_double), ("sum_bb", ctypes.c_double),
+                ("cosine", ctypes.c_double), ("pairs", ctypes.c_uint64), ("blocks", ctypes.c_uint64)]
+
+
 class GuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
                 ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
@@ -79,6 +84,7 @@ SEGMENT_RESULT_FIELDS = [f for f, _ in SegmentResult._fields_]
 GUARD_RESULT_FIELDS = [f for f, _ in GuardResult._fields_]
 
 EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments_ex",
+            "asmevo_diff_cosine", "asmevo_diff_cosine_workspace_bytes",
             "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
             "asmevo_abi_version", "asmevo_last_hip_error"]
 
@@ -110,6 +116,10 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_diff_segments_ex.argtypes = [P(Segment), ctypes.c_int32, vp, vp, ctypes.c_size_t, vp,
                                               ctypes.c_int32]
         L.asmevo_diff_segments_ex.restype = ctypes.c_int32
+        L.asmevo_diff_cosine.argtypes = [P(Segment), ctypes.c_int32, vp, vp, vp, ctypes.c_size_t, vp]
+        L.asmevo_diff_cosine.restype = ctypes.c_int32
+        L.asmevo_diff_cosine_workspace_bytes.argtypes = [P(Segment), ctypes.c_int32]
+        L.asmevo_diff_cosine_workspace_bytes.restype = ctypes.c_size_t
         L.asmevo_guard_check.argtypes = [P(Alloc), ctypes.c_int32, ctypes.c_uint64, vp, vp,
                                          ctypes.c_size_t, vp]
         L.asmevo_guard_check.restype = ctypes.c_int32
@@ -168,6 +178,19 @@ def diff_segments(segments: Sequence[Segment], results_ptr: int, workspace_ptr: 
     _check(_lib().asmevo_diff_segments_ex(s, len(segments), results_ptr, workspace_ptr,
                                           workspace_size, _stream_handle(stream), workgroups),
            "asmevo_diff_segments")
+
+
+def diff_cosine_workspace_bytes(segments: Sequence[Segment]) -> int:
+    s = _array(Segment, segments)
+    return int(_lib().asmevo_diff_cosine_workspace_bytes(s, len(segments)))
+
+
+def diff_cosine(segments: Sequence[Segment], results_ptr: int, cos_results_ptr: int, workspace_ptr: int,
+                workspace_size: int, stream=None) -> None:
+    s = _array(Segment, segments)
+    _check(_lib().asmevo_diff_cosine(s, len(segments), results_ptr, cos_results_ptr, workspace_ptr,
+                                     workspace_size, _stream_handle(stream)),
+           "asmevo_diff_cosine")
 
 
 def guard_check(allocs: Sequence[Alloc], seed: int, results_ptr: int, workspace_ptr: int,

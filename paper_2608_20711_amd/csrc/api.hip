@@ -249,13 +249,17 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
 }
 
 // ---------------------------------------------------------------------------
-asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
-                                      asmevo_segment_result* results, void* workspace,
-                                      size_t ws_bytes, void* stream, int32_t workgroups) {
-  if (n < 0 || (n > 0 && (!segs || !results)) || workgroups < 0) return ASMEVO_E_INVALID;
-  if (n == 0) return ASMEVO_OK;
-  std::vector<DiffSeg> dev(n);
-  uint64_t tiles = 0;
+}  // extern "C"
+
+namespace {
+
+// Validates the segments and builds their device descriptors.  `row_tiled`
+// keeps every tile inside one row (the cosine's 4096-byte blocks).
+asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled,
+                        std::vector<DiffSeg>& dev, uint64_t& tiles) {
+  if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
+  dev.assign((size_t)n, DiffSeg{});
+  tiles = 0;
   for (int32_t k = 0; k < n; ++k) {
     const asmevo_segment& S = segs[k];
     const int es = esize_of(S.dtype);
@@ -286,33 +290,61 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
     D.esize = (uint32_t)es;
     D.result_index = (uint32_t)k;
     D.tile_begin = tiles;
-    if (!empty) {
-      const bool flat = S.rows == 1 || (S.stride_a == S.cols && S.stride_b == S.cols);
-      D.rows = flat ? 1 : (uint64_t)S.rows;
-      D.cols = flat ? (uint64_t)(S.rows * S.cols) : (uint64_t)S.cols;
-      D.a_pitch = (uint64_t)S.stride_a * es;
-      D.b_pitch = (uint64_t)S.stride_b * es;
-      D.row_bytes = D.cols * es;
-      D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
-      D.full_chunks = D.row_bytes / kChunk;
-      const bool aligned = (S.a % 16 == 0) && (S.b % 16 == 0) &&
-                           (D.rows == 1 || (D.a_pitch % 16 == 0 && D.b_pitch % 16 == 0));
-      const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
-      D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) |
-                ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
-      if (narrow) {
-        D.tiles_per_row = 0;
-        D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
-      } else {
-        const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;
-        D.tile_count = D.rows * tpr;
-        // 2-D row-tiled segments index tiles in 32 bits
-        if (D.rows > 1 && (D.tile_count >> 32) != 0) return ASMEVO_E_INVALID;
-        D.tiles_per_row = (uint32_t)(tpr > 0xFFFFFFFFull ? 0xFFFFFFFFull : tpr);
-      }
-      tiles += D.tile_count;
+    if (empty) continue;
+    const bool flat = S.rows == 1 || (S.stride_a == S.cols && S.stride_b == S.cols);
+    D.rows = flat ? 1 : (uint64_t)S.rows;
+    D.cols = flat ? (uint64_t)(S.rows * S.cols) : (uint64_t)S.cols;
+    D.a_pitch = (uint64_t)S.stride_a * es;
+    D.b_pitch = (uint64_t)S.stride_b * es;
+    D.row_bytes = D.cols * es;
+    D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
+    D.full_chunks = D.row_bytes / kChunk;
+    const bool aligned = (S.a % 16 == 0) && (S.b % 16 == 0) &&
+                         (D.rows == 1 || (D.a_pitch % 16 == 0 && D.b_pitch % 16 == 0));
+    const bool narrow = !row_tiled && D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
+    D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) |
+              ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
+    if (narrow) {
+      D.tiles_per_row = 0;
+      D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
+    } else {
+      const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;
+      D.tile_count = D.rows * tpr;
+      // 2-D row-tiled segments index tiles in 32 bits
+      if (D.rows > 1 && (D.tile_count >> 32) != 0) return ASMEVO_E_INVALID;
+      D.tiles_per_row = (uint32_t)(tpr > 0xFFFFFFFFull ? 0xFFFFFFFFull : tpr);
     }
+    tiles += D.tile_count;
   }
+  return ASMEVO_OK;
+}
+
+// Cosine workspace: descriptors | one non-finite pair counter per segment |
+// three doubles per tile.
+struct CosLayout {
+  size_t off_counters, off_partials, bytes;
+};
+CosLayout cos_layout(int32_t n, uint64_t tiles) {
+  CosLayout L;
+  L.off_counters = align256((size_t)n * sizeof(DiffSeg));
+  L.off_partials = L.off_counters + align256((size_t)n * sizeof(uint64_t));
+  L.bytes = L.off_partials + (size_t)tiles * 3 * sizeof(double);
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
+                                      asmevo_segment_result* results, void* workspace,
+                                      size_t ws_bytes, void* stream, int32_t workgroups) {
+  if (n < 0 || (n > 0 && (!segs || !results)) || workgroups < 0) return ASMEVO_E_INVALID;
+  if (n == 0) return ASMEVO_OK;
+  std::vector<DiffSeg> dev;
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff(segs, n, false, dev, tiles);
+  if (st != ASMEVO_OK) return st;
   const size_t bytes = dev.size() * sizeof(DiffSeg);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -327,6 +359,34 @@ asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
                                    asmevo_segment_result* results, void* workspace,
                                    size_t ws_bytes, void* stream) {
   return asmevo_diff_segments_ex(segs, n, results, workspace, ws_bytes, stream, 0);
+}
+
+size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n) {
+  std::vector<DiffSeg> dev;
+  uint64_t tiles = 0;
+  if (n <= 0 || plan_diff(segs, n, true, dev, tiles) != ASMEVO_OK) return 0;
+  return cos_layout(n, tiles).bytes;
+}
+
+asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
+                                 asmevo_segment_result* results, asmevo_cosine_result* cos_results,
+                                 void* workspace, size_t ws_bytes, void* stream) {
+  if (n < 0 || (n > 0 && (!segs || !results || !cos_results))) return ASMEVO_E_INVALID;
+  if (n == 0) return ASMEVO_OK;
+  std::vector<DiffSeg> dev;
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff(segs, n, true, dev, tiles);
+  if (st != ASMEVO_OK) return st;
+  const CosLayout L = cos_layout(n, tiles);
+  if (!workspace || ws_bytes < L.bytes) return ASMEVO_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  HIP_TRY(hipMemcpyAsync(ws, dev.data(), dev.size() * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
+  const int wg = device_cus() * diff_blocks_per_cu();
+  HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(ws), n, tiles, results, wg, s,
+                      reinterpret_cast<double*>(ws + L.off_partials),
+                      reinterpret_cast<unsigned long long*>(ws + L.off_counters), cos_results));
+  return ASMEVO_OK;
 }
 
 // ---------------------------------------------------------------------------

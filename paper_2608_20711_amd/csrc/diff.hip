@@ -1,21 +1,27 @@
 // diff.hip -- segmented multi-buffer comparison of a candidate state against
 // the reference state (AsmEvo section 3.2, Eq. 1: Delta = K'(x) - O(x) and
-// its infinity norm; iota: bit-exact integer buffers; section 3.4: floating
-// outputs by tolerance, integer / opaque state byte-exactly).
+// its infinity norm, and the cosine c_x = cos(K'(x), O(x)); iota: bit-exact
+// integer buffers; section 3.4: floating outputs by tolerance, integer /
+// opaque state byte-exactly).
 //
 // Streaming, HBM-bound design for gfx950:
-//  * every segment is cut into tiles of 512 16-byte chunks (8 KiB per
-//    operand); all segments share one flat tile space;
-//  * each wave owns a contiguous range of tiles and issues 8 non-temporal
+//  * every segment is cut into tiles of 256 16-byte chunks (4 KiB per
+//    operand), each inside one row; all segments share one flat tile space;
+//  * each wave owns a contiguous range of tiles and issues 4 non-temporal
 //    dwordx4 loads per operand per lane before looking at any of them;
-//  * the common case is a 128-bit XOR that is zero: nothing else runs;
+//  * the common case is a 128-bit XOR that is zero: one combined check per
+//    tile, nothing else runs;
 //  * only chunks whose bits differ (or, under the strict NaN policy, hold a
 //    NaN) are decoded and tested in fp64;
 //  * per-lane partials are reduced across the wave with cross-lane shuffles
 //    only when the wave has seen a difference in the segment it leaves, and
 //    land in the result with exact 64-bit atomics (sum / min / max of
 //    non-negative doubles as bit patterns), so results are identical for any
-//    schedule or launch geometry.
+//    schedule or launch geometry;
+//  * the cosine variant also accumulates fp64 a*b, a*a, b*b per lane over the
+//    same registers, folds each tile (= one 4096-byte block) with an xor
+//    butterfly and stores the block sums; cosine_kernel folds the blocks of a
+//    segment with the left-complete pairwise tree.
 #include "device_math.h"
 #include "kernels.h"
 #include "layout.h"
@@ -197,20 +203,123 @@ __device__ __forceinline__ void load_chunk(const uint8_t* pa, const uint8_t* pb,
   }
 }
 
-// All tiles [t_begin, t_end) of one segment.
+// ------------------------------------------------------------ cosine sums
+// Lane sums of one 4096-byte block (a*b, a*a, b*b over pairs with both
+// values finite).  Products of two values of any float element type are
+// exact in fp64, so fma(A, B, s) rounds exactly like s + A*B.
+struct Cos {
+  double ab, aa, bb;
+};
+
+// Exact fp64 value of finite element e (a compile-time position) of a chunk,
+// through the hardware conversions: bf16 by a shift into binary32, fp16 by
+// v_cvt_f32_f16 (exact, subnormals kept), fp8 e4m3 by v_cvt_f32_fp8 (the
+// OCP E4M3FN decode on gfx950, checked against the oracle for all 256
+// patterns), then binary32 -> binary64, which is exact.
 template <int DT>
+__device__ __forceinline__ double elem_f64(const u32x4& v, int e) {
+  if constexpr (DT == ASMEVO_F32) {
+    return (double)__uint_as_float(v[e]);
+  } else if constexpr (DT == ASMEVO_BF16) {
+    const uint32_t w = v[e >> 1];
+    return (double)__uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  } else if constexpr (DT == ASMEVO_F16) {
+    const uint16_t h = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    return (double)(float)__builtin_bit_cast(_Float16, h);
+  } else {
+    const int w = (int)v[e >> 2];
+    switch (e & 3) {   // the byte selector must be a literal
+      case 0: return (double)__builtin_amdgcn_cvt_f32_fp8(w, 0);
+      case 1: return (double)__builtin_amdgcn_cvt_f32_fp8(w, 1);
+      case 2: return (double)__builtin_amdgcn_cvt_f32_fp8(w, 2);
+      default: return (double)__builtin_amdgcn_cvt_f32_fp8(w, 3);
+    }
+  }
+}
+
+// Does any element of the chunk have an all-ones exponent (Inf or NaN)?
+template <int DT>
+__device__ __forceinline__ bool any_nonfinite(const u32x4& v) {
+  uint32_t hit = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t w = v[k];
+    if constexpr (DT == ASMEVO_F32) {
+      hit |= ((w & 0x7F800000u) == 0x7F800000u) ? 1u : 0u;
+    } else if constexpr (DT == ASMEVO_BF16 || DT == ASMEVO_F16) {
+      constexpr uint32_t e = DT == ASMEVO_BF16 ? 0x7F80u : 0x7C00u;
+      hit |= ((w & e) == e) ? 1u : 0u;
+      hit |= (((w >> 16) & e) == e) ? 1u : 0u;
+    } else {
+      // fp8 e4m3: only S.1111.111 is not finite
+      const uint32_t m = w & 0x7F7F7F7Fu;
+      const uint32_t t = m ^ 0x7F7F7F7Fu;            // a zero byte where the pattern is 0x7F
+      hit |= ((t - 0x01010101u) & ~t & 0x80808080u) ? 1u : 0u;
+    }
+  }
+  return hit != 0;
+}
+
+template <int DT>
+__device__ __forceinline__ void cos_chunk(const u32x4& va, const u32x4& vb, uint32_t nvalid, Cos& c,
+                                          uint32_t& nonfinite) {
+  constexpr int epc = 16 / Et<DT>::es;
+  if (nvalid == (uint32_t)epc && !any_nonfinite<DT>(va) && !any_nonfinite<DT>(vb)) {
+#pragma unroll
+    for (int e = 0; e < epc; ++e) {
+      const double A = elem_f64<DT>(va, e);
+      const double B = elem_f64<DT>(vb, e);
+      c.ab = __builtin_fma(A, B, c.ab);
+      c.aa = __builtin_fma(A, A, c.aa);
+      c.bb = __builtin_fma(B, B, c.bb);
+    }
+    return;
+  }
+#pragma unroll 1
+  for (uint32_t e = 0; e < nvalid; ++e) {
+    double A = 0.0, B = 0.0;
+    if (decode<DT>(elem_dyn<DT>(va, e), A) != 0 || decode<DT>(elem_dyn<DT>(vb, e), B) != 0) {
+      nonfinite += 1;
+      continue;
+    }
+    c.ab = __builtin_fma(A, B, c.ab);
+    c.aa = __builtin_fma(A, A, c.aa);
+    c.bb = __builtin_fma(B, B, c.bb);
+  }
+}
+
+// Folds the lane sums of a block by the xor butterfly and stores them.
+__device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    c.ab = c.ab + __shfl_xor(c.ab, m, kWave);
+    c.aa = c.aa + __shfl_xor(c.aa, m, kWave);
+    c.bb = c.bb + __shfl_xor(c.bb, m, kWave);
+  }
+  if (lane == 0) {
+    out[0] = c.ab;
+    out[1] = c.aa;
+    out[2] = c.bb;
+  }
+}
+
+// All tiles [t_begin, t_end) of one segment.  COS: also the block sums of
+// each tile into `partials` (three doubles per global tile index).
+template <int DT, bool COS>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, uint64_t t_end,
-                                           uint32_t lane, Acc& acc) {
+                                           uint32_t lane, Acc& acc, double* partials,
+                                           uint32_t& nonfinite) {
   constexpr int es = Et<DT>::es;
   constexpr int epc = 16 / es;
   constexpr int U = kDiffUnroll;
+  constexpr bool kCos = COS && Et<DT>::fp;
   const bool tol_mode = S.mode == ASMEVO_TOLERANCE;
   const bool strict = (S.flags & kSegStrict) != 0;
   const bool vec = (S.flags & kSegVec) != 0;
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
 
-  if (S.flags & kSegNarrow) {
+  if (!kCos && (S.flags & kSegNarrow)) {
     // Short rows: tiles over the row-major chunk space, each lane finds its row.
     const uint64_t total = S.rows * S.row_chunks;
     for (uint64_t tile = t_begin; tile < t_end; ++tile) {
@@ -236,53 +345,9 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
     return;
   }
 
-  // Row-tiled: every tile lies inside one row.
+  // Row-tiled: every tile lies inside one row (and is one cosine block).
   const uint64_t tpr = S.tiles_per_row;
-  uint64_t tile = t_begin;
-#if ASMEVO_DIFF_PIPELINE
-  if (S.rows == 1 && vec) {
-    // Contiguous segment: its whole tiles run as a software pipeline -- the
-    // loads of tile t+1 are in flight while tile t is checked.
-    const uint64_t whole = S.full_chunks / kTileChunks;
-    const uint64_t t_fast = t_end < whole ? t_end : whole;
-    if (tile < t_fast) {
-      const uint8_t* qa = a0 + (uint64_t)lane * kChunk;
-      const uint8_t* qb = b0 + (uint64_t)lane * kChunk;
-      u32x4 va[U], vb[U];
-#pragma unroll
-      for (int j = 0; j < U; ++j) {
-        va[j] = ld_nt(qa + (tile * kTileChunks + j * kWave) * kChunk);
-        vb[j] = ld_nt(qb + (tile * kTileChunks + j * kWave) * kChunk);
-      }
-      for (; tile < t_fast; ++tile) {
-        u32x4 na[U], nb[U];
-        if (tile + 1 < t_fast) {
-#pragma unroll
-          for (int j = 0; j < U; ++j) {
-            na[j] = ld_nt(qa + ((tile + 1) * kTileChunks + j * kWave) * kChunk);
-            nb[j] = ld_nt(qb + ((tile + 1) * kTileChunks + j * kWave) * kChunk);
-          }
-        }
-        u32x4 x = va[0] ^ vb[0];
-#pragma unroll
-        for (int j = 1; j < U; ++j) x |= va[j] ^ vb[j];
-        if (((x.x | x.y | x.z | x.w) != 0u) || strict) {
-          const uint64_t k0 = tile * (uint64_t)kTileChunks;
-#pragma unroll
-          for (int j = 0; j < U; ++j)
-            chunk<DT>(va[j], vb[j], (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode, strict,
-                      S.atol, S.rtol, acc);
-        }
-#pragma unroll
-        for (int j = 0; j < U; ++j) {
-          va[j] = na[j];
-          vb[j] = nb[j];
-        }
-      }
-    }
-  }
-#endif
-  for (; tile < t_end; ++tile) {
+  for (uint64_t tile = t_begin; tile < t_end; ++tile) {
     uint64_t r = 0, kt = tile;
     if (S.rows > 1) {
       r = (uint32_t)tile / (uint32_t)tpr;
@@ -292,6 +357,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
     const uint8_t* pb = b0 + r * S.b_pitch;
     const uint64_t ibase = r * S.cols;
     const uint64_t k0 = kt * (uint64_t)kTileChunks;
+    Cos cs{0.0, 0.0, 0.0};
     if (vec && k0 + kTileChunks <= S.full_chunks) {
       // Whole tile: issue all loads first, then one combined check.
       const uint8_t* qa = pa + (k0 + lane) * kChunk;
@@ -311,6 +377,11 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
           chunk<DT>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
                     strict, S.atol, S.rtol, acc);
       }
+      if constexpr (kCos) {
+#pragma unroll
+        for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], epc, cs, nonfinite);
+        cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);
+      }
       continue;
     }
     // Last tile of a row (or misaligned operands): per-chunk bounds.
@@ -326,7 +397,9 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
         load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
       }
       chunk<DT>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
+      if constexpr (kCos) cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
     }
+    if constexpr (kCos) cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);
   }
 }
 
@@ -354,7 +427,14 @@ __device__ __forceinline__ uint64_t wave_max(uint64_t v) {
 
 // Folds the wave's partials for one segment into its result (only if the
 // wave saw anything) and resets them.
-__device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment_result* results, uint32_t lane) {
+__device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment_result* results,
+                                      uint32_t lane, uint32_t& nonfinite,
+                                      unsigned long long* nonfinite_pairs) {
+  if (nonfinite_pairs != nullptr && __ballot(nonfinite != 0u) != 0ull) {
+    const uint64_t nfp = wave_sum(nonfinite);
+    if (lane == 0) atomicAdd(nonfinite_pairs + S.result_index, (unsigned long long)nfp);
+    nonfinite = 0;
+  }
   if (__ballot((acc.bw | acc.tol) != 0u) == 0ull) return;
   uint64_t bw = wave_sum(acc.bw);
   uint64_t tol = wave_sum(acc.tol);
@@ -384,9 +464,11 @@ __device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment
   acc_reset(acc);
 }
 
-__global__ void diff_init_kernel(asmevo_segment_result* results, int n) {
+__global__ void diff_init_kernel(asmevo_segment_result* results, int n,
+                                 unsigned long long* nonfinite_pairs) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n) return;
+  if (nonfinite_pairs != nullptr) nonfinite_pairs[t] = 0;
   asmevo_segment_result r;
   r.mismatches = 0;
   r.first_mismatch = -1;
@@ -399,10 +481,12 @@ __global__ void diff_init_kernel(asmevo_segment_result* results, int n) {
 }
 
 
-__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(ASMEVO_DIFF_WAVES_PER_EU)))
-void diff_kernel(const DiffSeg* __restrict__ segs, int n,
-                                                          uint64_t total_tiles,
-                                                          asmevo_segment_result* results) {
+template <bool COS>
+__global__ __launch_bounds__(kDiffBlock)
+__attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU : ASMEVO_DIFF_WAVES_PER_EU)))
+void diff_kernel(const DiffSeg* __restrict__ segs, int n, uint64_t total_tiles,
+                 asmevo_segment_result* results, double* partials,
+                 unsigned long long* nonfinite_pairs) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = (uint64_t)blockIdx.x * (kDiffBlock / kWave) +
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -419,6 +503,7 @@ void diff_kernel(const DiffSeg* __restrict__ segs, int n,
   int s = s_lo;
   Acc acc;
   acc_reset(acc);
+  uint32_t nonfinite = 0;
   uint64_t t = lo;
   while (t < hi) {
     while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
@@ -427,16 +512,119 @@ void diff_kernel(const DiffSeg* __restrict__ segs, int n,
     const uint64_t t_end = seg_end < hi ? seg_end : hi;
     const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
     switch (S.dtype) {
-      case ASMEVO_F32: diff_range<ASMEVO_F32>(S, b, e, lane, acc); break;
-      case ASMEVO_BF16: diff_range<ASMEVO_BF16>(S, b, e, lane, acc); break;
-      case ASMEVO_F16: diff_range<ASMEVO_F16>(S, b, e, lane, acc); break;
-      case ASMEVO_FP8_E4M3: diff_range<ASMEVO_FP8_E4M3>(S, b, e, lane, acc); break;
-      case ASMEVO_I32: diff_range<ASMEVO_I32>(S, b, e, lane, acc); break;
-      case ASMEVO_I64: diff_range<ASMEVO_I64>(S, b, e, lane, acc); break;
-      default: diff_range<ASMEVO_U8>(S, b, e, lane, acc); break;
+      case ASMEVO_F32: diff_range<ASMEVO_F32, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_F16: diff_range<ASMEVO_F16, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_FP8_E4M3: diff_range<ASMEVO_FP8_E4M3, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_I32: diff_range<ASMEVO_I32, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_I64: diff_range<ASMEVO_I64, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      default: diff_range<ASMEVO_U8, COS>(S, b, e, lane, acc, partials, nonfinite); break;
     }
-    flush(acc, S, results, lane);
+    flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
     t = t_end;
+  }
+}
+
+// One workgroup per segment: the left-complete pairwise tree over the
+// segment's block sums, as a binary counter -- aligned groups of 256 blocks
+// are perfect trees reduced in LDS, the remaining blocks are pushed one by
+// one; the counter's perfect trees, largest first, are then folded from the
+// right, which is exactly P(x[0..n)) = P(x[0..h)) + P(x[h..n)).
+constexpr int kCosBlock = 256;
+
+__global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __restrict__ segs,
+                                                           const double* __restrict__ partials,
+                                                           const unsigned long long* nonfinite_pairs,
+                                                           asmevo_cosine_result* out) {
+  const int s = blockIdx.x;
+  const DiffSeg S = segs[s];
+  __shared__ double v[3][kCosBlock];
+  __shared__ double stack_val[3][64];
+  __shared__ int stack_lvl[64];
+  __shared__ int depth;
+  const int t = threadIdx.x;
+  if (!(S.dtype >= ASMEVO_F32 && S.dtype <= ASMEVO_FP8_E4M3)) {
+    if (t == 0) {
+      asmevo_cosine_result r;
+      r.sum_ab = r.sum_aa = r.sum_bb = 0.0;
+      r.cosine = __builtin_nan("");
+      r.pairs = 0;
+      r.blocks = 0;
+      out[S.result_index] = r;
+    }
+    return;
+  }
+  if (t == 0) depth = 0;
+  __syncthreads();
+  // push (value, level) onto the counter, merging equal levels (left + right)
+  auto push = [&](double ab, double aa, double bb, int lvl) {
+    while (depth > 0 && stack_lvl[depth - 1] == lvl) {
+      ab = stack_val[0][depth - 1] + ab;
+      aa = stack_val[1][depth - 1] + aa;
+      bb = stack_val[2][depth - 1] + bb;
+      --depth;
+      ++lvl;
+    }
+    stack_val[0][depth] = ab;
+    stack_val[1][depth] = aa;
+    stack_val[2][depth] = bb;
+    stack_lvl[depth] = lvl;
+    ++depth;
+  };
+  const uint64_t nb = S.tile_count;
+  const double* p = partials + 3 * S.tile_begin;
+  uint64_t g = 0;
+  for (; g + kCosBlock <= nb; g += kCosBlock) {
+    v[0][t] = p[3 * (g + t) + 0];
+    v[1][t] = p[3 * (g + t) + 1];
+    v[2][t] = p[3 * (g + t) + 2];
+    __syncthreads();
+    for (int width = kCosBlock / 2; width >= 1; width >>= 1) {
+      double ab = 0.0, aa = 0.0, bb = 0.0;
+      if (t < width) {
+        ab = v[0][2 * t] + v[0][2 * t + 1];
+        aa = v[1][2 * t] + v[1][2 * t + 1];
+        bb = v[2][2 * t] + v[2][2 * t + 1];
+      }
+      __syncthreads();
+      if (t < width) {
+        v[0][t] = ab;
+        v[1][t] = aa;
+        v[2][t] = bb;
+      }
+      __syncthreads();
+    }
+    if (t == 0) push(v[0][0], v[1][0], v[2][0], 8);
+    __syncthreads();
+  }
+  if (t == 0) {
+    for (; g < nb; ++g) push(p[3 * g + 0], p[3 * g + 1], p[3 * g + 2], 0);
+    double ab = 0.0, aa = 0.0, bb = 0.0;
+    if (depth > 0) {
+      ab = stack_val[0][depth - 1];
+      aa = stack_val[1][depth - 1];
+      bb = stack_val[2][depth - 1];
+      for (int k = depth - 2; k >= 0; --k) {
+        ab = stack_val[0][k] + ab;
+        aa = stack_val[1][k] + aa;
+        bb = stack_val[2][k] + bb;
+      }
+    }
+    asmevo_cosine_result r;
+    r.sum_ab = ab;
+    r.sum_aa = aa;
+    r.sum_bb = bb;
+    if (aa == 0.0 && bb == 0.0) r.cosine = 1.0;
+    else if (aa == 0.0 || bb == 0.0) r.cosine = 0.0;
+    else {
+      const double na = __builtin_sqrt(aa);
+      const double nbb = __builtin_sqrt(bb);
+      const double den = na * nbb;
+      r.cosine = ab / den;
+    }
+    r.pairs = S.rows * S.cols - nonfinite_pairs[S.result_index];
+    r.blocks = nb;
+    out[S.result_index] = r;
   }
 }
 
@@ -444,23 +632,41 @@ void diff_kernel(const DiffSeg* __restrict__ segs, int n,
 
 int diff_blocks_per_cu() {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel, kDiffBlock, 0) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false>, kDiffBlock, 0) !=
+          hipSuccess ||
       blocks <= 0)
     blocks = 4;
   return blocks;
 }
 
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
-                       asmevo_segment_result* results, int workgroups, hipStream_t stream) {
+                       asmevo_segment_result* results, int workgroups, hipStream_t stream,
+                       double* partials, unsigned long long* nonfinite_pairs,
+                       asmevo_cosine_result* cos_results) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(diff_init_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, results, n);
+  const bool cos = cos_results != nullptr;
+  hipLaunchKernelGGL(diff_init_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, results, n,
+                     cos ? nonfinite_pairs : nullptr);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || total_tiles == 0) return e;
-  const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
-  const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
-  hipLaunchKernelGGL(diff_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n, total_tiles,
-                     results);
-  return hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (total_tiles > 0) {
+    const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
+    const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
+    if (cos)
+      hipLaunchKernelGGL(diff_kernel<true>, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n, total_tiles,
+                         results, partials, nonfinite_pairs);
+    else
+      hipLaunchKernelGGL(diff_kernel<false>, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n,
+                         total_tiles, results, nullptr, nullptr);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (cos) {
+    hipLaunchKernelGGL(cosine_kernel, dim3(n), dim3(kCosBlock), 0, stream, segs, partials,
+                       nonfinite_pairs, cos_results);
+    e = hipGetLastError();
+  }
+  return e;
 }
 
 }  // namespace asmevo

@@ -15,8 +15,12 @@ hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_p
 
 // Resident diff workgroups per compute unit (from the occupancy calculator).
 int diff_blocks_per_cu();
+// Diff of all segments; with cos_results, also the cosine term (partials:
+// three doubles per tile; nonfinite_pairs: one counter per segment).
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
-                       asmevo_segment_result* results, int workgroups, hipStream_t stream);
+                       asmevo_segment_result* results, int workgroups, hipStream_t stream,
+                       double* partials = nullptr, unsigned long long* nonfinite_pairs = nullptr,
+                       asmevo_cosine_result* cos_results = nullptr);
 
 hipError_t launch_guard(const GuardRegion* regs, int n_regs, uint64_t total_chunks, uint64_t seed,
                         asmevo_guard_result* results, int n_results, hipStream_t stream);

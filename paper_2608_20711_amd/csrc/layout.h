@@ -19,6 +19,9 @@ constexpr int kDiffUnroll = ASMEVO_DIFF_UNROLL;      // chunks per lane per tile
 #ifndef ASMEVO_DIFF_WAVES_PER_EU                     // occupancy target of the diff kernel
 #define ASMEVO_DIFF_WAVES_PER_EU 4
 #endif
+#ifndef ASMEVO_COS_WAVES_PER_EU                      // ... and of its cosine variant
+#define ASMEVO_COS_WAVES_PER_EU 3
+#endif
 constexpr int kTileChunks = kWave * kDiffUnroll;     // 256 chunks = 4 KiB per operand
 constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
 

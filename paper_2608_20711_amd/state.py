@@ -13,12 +13,14 @@ import numpy as np
 import torch
 
 from . import (Alloc, DIST_CODE, DTYPE_CODE, FILL_SATURATE, Injection, KIND_CODE, MODE_CODE,
-               NAN_CODE, INJ_RATE, SIDE_CODE, Segment, diff_segments, fill_guarded, guard_check,
-               workspace_bytes)
+               NAN_CODE, INJ_RATE, SIDE_CODE, Segment, diff_cosine, diff_cosine_workspace_bytes,
+               diff_segments, fill_guarded, guard_check, workspace_bytes)
 
 SEG_RESULT_DTYPE = np.dtype([("mismatches", "<u8"), ("first_mismatch", "<i8"),
                              ("bitwise_mismatches", "<u8"), ("first_bitwise", "<i8"),
                              ("nonfinite_mismatches", "<u8"), ("max_abs", "<f8"), ("max_rel", "<f8")])
+COS_RESULT_DTYPE = np.dtype([("sum_ab", "<f8"), ("sum_aa", "<f8"), ("sum_bb", "<f8"), ("cosine", "<f8"),
+                             ("pairs", "<u8"), ("blocks", "<u8")])
 GUARD_RESULT_DTYPE = np.dtype([("bad_lo", "<u8"), ("bad_hi", "<u8"),
                                ("first_bad_lo", "<i8"), ("first_bad_hi", "<i8")])
 
@@ -52,6 +54,9 @@ class DeviceState:
         self.allocs_ref = self._alloc_structs(self.ref)
         self.allocs_cand = self._alloc_structs(self.cand)
         self.segments = self._segment_structs()
+        self.cos_ws = None
+        self.cos_res = torch.empty(max(1, len(w.compares)) * COS_RESULT_DTYPE.itemsize,
+                                   dtype=torch.uint8, device=self.device)
 
     def arena(self, side: str) -> torch.Tensor:
         return self.cand if side == "cand" else self.ref
@@ -84,6 +89,20 @@ class DeviceState:
     def diff(self, stream=None, workgroups: int = 0, segments: Optional[List[Segment]] = None) -> None:
         diff_segments(segments if segments is not None else self.segments, self.seg_res.data_ptr(),
                       self.ws.data_ptr(), self.ws_size, stream, workgroups)
+
+    def diff_cosine(self, stream=None) -> None:
+        """The diff plus the cosine term of every float segment, in one pass."""
+        if self.cos_ws is None:
+            size = diff_cosine_workspace_bytes(self.segments)
+            self.cos_ws = torch.empty(max(size, 256), dtype=torch.uint8, device=self.device)
+        diff_cosine(self.segments, self.seg_res.data_ptr(), self.cos_res.data_ptr(), self.cos_ws.data_ptr(),
+                    self.cos_ws.numel(), stream)
+
+    def cos_results(self) -> List[Dict]:
+        torch.cuda.synchronize(self.device)
+        n = len(self.w.compares)
+        raw = self.cos_res.cpu().numpy()[: n * COS_RESULT_DTYPE.itemsize].view(COS_RESULT_DTYPE)
+        return [{f: raw[f][k].item() for f in COS_RESULT_DTYPE.names} for k in range(n)]
 
     def guard(self, stream=None) -> None:
         guard_check(self.allocs_cand, self.w.seed, self.guard_res.data_ptr(), self.ws.data_ptr(),

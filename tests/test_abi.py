@@ -38,6 +38,7 @@ def test_struct_layouts_match_header(tmp_path):
     fields = {
         "asmevo_alloc": lib.Alloc, "asmevo_injection": lib.Injection, "asmevo_segment": lib.Segment,
         "asmevo_segment_result": lib.SegmentResult, "asmevo_guard_result": lib.GuardResult,
+        "asmevo_cosine_result": lib.CosineResult,
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "asmevo.h"', "int main(void) {"]
     for cname, cls in fields.items():
@@ -162,3 +163,19 @@ def test_guard_argument_errors():
     with pytest.raises(lib.AsmevoError) as e:
         lib.guard_check([_alloc()], 1, 0x40000, 0x50000, 4, stream=0)
     assert e.value.status == lib.E_WORKSPACE
+
+
+def test_cosine_workspace_and_errors():
+    L = lib.lib()
+    segs = (lib.Segment * 2)(_seg(), _seg(rows=3, cols=1000, stride_a=1024, stride_b=1024))
+    need = L.asmevo_diff_cosine_workspace_bytes(segs, 2)
+    # descriptors + counters + 3 doubles per 4096-byte block (1 + 3 blocks)
+    assert need >= 2 * 128 + 2 * 8 + 4 * 24
+    bad = (lib.Segment * 1)(_seg(dtype=99))
+    assert L.asmevo_diff_cosine_workspace_bytes(bad, 1) == 0
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_cosine([_seg()], 0x40000, 0x48000, 0x50000, 16, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_cosine([_seg()], 0x40000, 0, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID

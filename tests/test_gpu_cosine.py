@@ -1,0 +1,120 @@
+"""GPU parity of the cosine term of Eq. 1 (c = cos(K'(x), O(x)) per buffer):
+the HIP diff+cosine pass against the CPU oracle, bit for bit on the three fp64
+sums, the cosine and the pair counts, on the workloads and on odd layouts.
+The diff results of the same pass must equal those of the plain diff."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_20711_amd as lib
+import workloads
+from gpu_helpers import THREADS, assert_results_equal, log, run_gpu
+from paper_2608_20711_amd.state import COS_RESULT_DTYPE, SEG_RESULT_DTYPE
+from workloads import ESIZE
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name", list(workloads.ALL))
+def test_cosine_reduced_workloads(name):
+    w = workloads.ALL[name](small=True)
+    st = run_gpu(w)
+    plain = st.seg_results()
+    st.diff_cosine()
+    got = st.cos_results()
+    assert st.seg_results() == plain                 # same diff results from the fused pass
+    cand, ref = st.arena_host("cand"), st.arena_host("ref")
+    assert_results_equal(got, oracle.cosine_workload(w, cand, ref, THREADS), f"{name} cosine")
+
+
+@pytest.mark.parametrize("name", ["single_fp32", "padded_bf16", "decode_state", "int_lowp"])
+def test_cosine_full_size(name):
+    w = workloads.ALL[name]()
+    log(f"[cosine full] {name}")
+    st = run_gpu(w)
+    plain = st.seg_results()
+    st.diff_cosine()
+    got = st.cos_results()
+    assert st.seg_results() == plain
+    cand, ref = st.arena_host("cand"), st.arena_host("ref")
+    assert_results_equal(got, oracle.cosine_workload(w, cand, ref, THREADS), f"{name} cosine")
+    for r, c in zip(got, w.compares):
+        if w.allocs[c.alloc].dtype in workloads.FLOAT_DTYPES:
+            assert r["cosine"] > 0.99
+
+
+def _cos_gpu(specs, a_d, b_d):
+    segs = [lib.Segment(a_d.data_ptr() + s["a_off"], b_d.data_ptr() + s["b_off"], lib.DTYPE_CODE[s["dtype"]],
+                        lib.BITWISE, 0, 0, s["rows"], s["cols"], s["sa"], s["sb"], 0.0, 0.0) for s in specs]
+    for s in specs:
+        for off, st, buf in ((s["a_off"], s["sa"], a_d), (s["b_off"], s["sb"], b_d)):
+            ext = 0 if s["rows"] == 0 or s["cols"] == 0 else ((s["rows"] - 1) * st + s["cols"]) * ESIZE[s["dtype"]]
+            assert off + ext <= buf.numel(), s
+    n = len(segs)
+    res = torch.empty(n * SEG_RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    cres = torch.empty(n * COS_RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    size = lib.diff_cosine_workspace_bytes(segs)
+    ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+    lib.diff_cosine(segs, res.data_ptr(), cres.data_ptr(), ws.data_ptr(), size)
+    torch.cuda.synchronize()
+    raw = cres.cpu().numpy().view(COS_RESULT_DTYPE)
+    return [{f: raw[f][k].item() for f in COS_RESULT_DTYPE.names} for k in range(n)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16", "fp8e4m3", "i32"])
+def test_cosine_layouts_and_specials(dtype):
+    rng = np.random.default_rng(17)
+    es = ESIZE[dtype]
+    nbytes = 2 << 20
+    n = nbytes // es
+    raw = rng.integers(0, 1 << (8 * es), size=2 * n, dtype=np.uint64)
+    if dtype in ("f32", "bf16", "f16", "fp8e4m3"):
+        # mostly ordinary values, a sprinkling of every special pattern
+        vals = (rng.standard_normal(2 * n) * 3).astype(np.float32)
+        if dtype == "f32":
+            raw = vals.view(np.uint32).astype(np.uint64)
+        elif dtype == "bf16":
+            raw = (vals.view(np.uint32) >> 16).astype(np.uint64)
+        elif dtype == "f16":
+            raw = vals.astype(np.float16).view(np.uint16).astype(np.uint64)
+        else:
+            raw = raw & 0x7F
+            raw[raw == 0x7F] = 0x3C
+        k = rng.integers(0, 2 * n, size=2 * n // 200)
+        raw[k] = rng.integers(0, 1 << (8 * es), size=k.size, dtype=np.uint64)   # any pattern, NaN/Inf included
+    npt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[es]
+    a_h = raw[:n].astype(npt).view(np.uint8).copy()
+    b_h = raw[n:].astype(npt).view(np.uint8).copy()
+    a_d, b_d = torch.from_numpy(a_h).cuda(), torch.from_numpy(b_h).cuda()
+    spec = lambda rows, cols, sa, sb, ao=0, bo=0: dict(dtype=dtype, rows=rows, cols=cols, sa=sa, sb=sb,
+                                                     a_off=ao, b_off=bo)
+    specs = [spec(1, n, n, n), spec(1, n - 5, n, n, es, 3 * es), spec(1, 4096 // es * 7 + 3, 0, 0),
+             spec(3, 1000, 1000, 1000), spec(41, 2000, 2048, 2048), spec(77, 1001, 1003, 1009, 0, es),
+             spec(300, 10, 13, 11), spec(1, 1, 1, 1, 7 * es, 9 * es), spec(0, 5, 5, 5)]
+    for s in specs:
+        s["sa"] = max(s["sa"], s["cols"])
+        s["sb"] = max(s["sb"], s["cols"])
+    got = _cos_gpu(specs, a_d, b_d)
+    want = [oracle.cosine_segment(dtype, s["rows"], s["cols"], s["sa"], s["sb"], a_h, b_h, s["a_off"],
+                                  s["b_off"]) for s in specs]
+    assert_results_equal(got, want, f"{dtype} cosine layouts")
+
+
+def test_cosine_every_fp8_and_f16_value():
+    """Single-block segments over every fp8 pattern and every fp16 pattern
+    (the GPU's element conversions against the oracle's decode)."""
+    a8 = np.arange(256, dtype=np.uint8)
+    b8 = np.roll(a8, 37).copy()
+    a16 = np.arange(1 << 16, dtype=np.uint16)
+    b16 = np.roll(a16, 1001).copy()
+    for dtype, a_h, b_h in (("fp8e4m3", a8, b8), ("f16", a16.view(np.uint8), b16.view(np.uint8))):
+        es = ESIZE[dtype]
+        n = a_h.size // es
+        a_d, b_d = torch.from_numpy(a_h.copy()).cuda(), torch.from_numpy(b_h.copy()).cuda()
+        per = 64 if dtype == "f16" else 16
+        specs = [dict(dtype=dtype, rows=1, cols=per, sa=per, sb=per, a_off=i * es, b_off=i * es)
+                 for i in range(0, n, per)]
+        got = _cos_gpu(specs, a_d, b_d)
+        want = [oracle.cosine_segment(dtype, 1, per, per, per, a_h, b_h, s["a_off"], s["b_off"]) for s in specs]
+        assert_results_equal(got, want, f"{dtype} every value")
