@@ -260,11 +260,31 @@ __device__ __forceinline__ bool any_nonfinite(const u32x4& v) {
   return hit != 0;
 }
 
+// Lane sums of one chunk with no checks: a NaN or Inf element makes a sum
+// non-finite (fp64 cannot overflow here: |a*b| < 2^256 and there are fewer
+// than 2^52 terms), which the caller detects to redo the block with checks.
 template <int DT>
-__device__ __forceinline__ void cos_chunk(const u32x4& va, const u32x4& vb, uint32_t nvalid, Cos& c,
-                                          uint32_t& nonfinite) {
+__device__ __forceinline__ void cos_chunk_fast(const u32x4& va, const u32x4& vb, Cos& c) {
   constexpr int epc = 16 / Et<DT>::es;
-  if (nvalid == (uint32_t)epc && !any_nonfinite<DT>(va) && !any_nonfinite<DT>(vb)) {
+  if constexpr (DT == ASMEVO_FP8_E4M3) {
+    // v_cvt_pk_f32_fp8: two bytes of a word per instruction
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      // the half selector must be a literal: low bytes first, then high bytes
+      const auto fa0 = __builtin_amdgcn_cvt_pk_f32_fp8((int)va[k], false);
+      const auto fb0 = __builtin_amdgcn_cvt_pk_f32_fp8((int)vb[k], false);
+      const auto fa1 = __builtin_amdgcn_cvt_pk_f32_fp8((int)va[k], true);
+      const auto fb1 = __builtin_amdgcn_cvt_pk_f32_fp8((int)vb[k], true);
+      const double A[4] = {(double)fa0[0], (double)fa0[1], (double)fa1[0], (double)fa1[1]};
+      const double B[4] = {(double)fb0[0], (double)fb0[1], (double)fb1[0], (double)fb1[1]};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c.ab = __builtin_fma(A[q], B[q], c.ab);
+        c.aa = __builtin_fma(A[q], A[q], c.aa);
+        c.bb = __builtin_fma(B[q], B[q], c.bb);
+      }
+    }
+  } else {
 #pragma unroll
     for (int e = 0; e < epc; ++e) {
       const double A = elem_f64<DT>(va, e);
@@ -273,8 +293,14 @@ __device__ __forceinline__ void cos_chunk(const u32x4& va, const u32x4& vb, uint
       c.aa = __builtin_fma(A, A, c.aa);
       c.bb = __builtin_fma(B, B, c.bb);
     }
-    return;
   }
+}
+
+// Lane sums of the first `nvalid` elements of a chunk, skipping (and
+// counting) pairs with a NaN or Inf.
+template <int DT>
+__device__ __forceinline__ void cos_chunk(const u32x4& va, const u32x4& vb, uint32_t nvalid, Cos& c,
+                                          uint32_t& nonfinite) {
 #pragma unroll 1
   for (uint32_t e = 0; e < nvalid; ++e) {
     double A = 0.0, B = 0.0;
@@ -379,7 +405,12 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
       }
       if constexpr (kCos) {
 #pragma unroll
-        for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], epc, cs, nonfinite);
+        for (int j = 0; j < U; ++j) cos_chunk_fast<DT>(va[j], vb[j], cs);
+        if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
+          cs = Cos{0.0, 0.0, 0.0};                 // this lane met a NaN or Inf: redo with checks
+#pragma unroll 1
+          for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], epc, cs, nonfinite);
+        }
         cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);
       }
       continue;
