@@ -58,6 +58,9 @@ def parse():
     p.add_argument("--cpu-sample-bytes", type=float, default=1.5 * 2 ** 30,
                    help="logical bytes per side of the oracle's sample")
     p.add_argument("--workgroups", type=int, default=0)
+    p.add_argument("--restore-steps", type=int, default=3,
+                   help="after the timed steps, time a Tier-2 restore of every buffer (guards "
+                        "included) from a snapshot, this many times (0: skip)")
     p.add_argument("--cosine-steps", type=int, default=5,
                    help="after the timed steps, time the diff + cosine pass (Eq. 1's c_x) this many "
                         "times on the last candidate and report it beside the metric (0: skip)")
@@ -215,6 +218,44 @@ def main():
                   "min_cosine": min((r["cosine"] for r in floats), default=None),
                   "diff_results_identical": seg_after == results,
                   "note": "one pass: diff + fp64 a*b, a*a, b*b per 4096-byte block, then the block tree"}
+    restore = None
+    if args.restore_steps > 0:
+        import paper_2608_20711_amd as lib
+        backup = torch.empty_like(st.cand)
+        spans = [(w.offsets[k], a.total_bytes) for k, a in enumerate(w.allocs)]
+        snap = [lib.Region(backup.data_ptr() + o, st.cand.data_ptr() + o, n) for o, n in spans]
+        rest = [lib.Region(st.cand.data_ptr() + o, backup.data_ptr() + o, n) for o, n in spans]
+        rws = torch.empty(lib.workspace_bytes(len(spans)), dtype=torch.uint8, device="cuda:0")
+        lib.copy_regions(snap, rws.data_ptr(), rws.numel(), stream)
+        torch.cuda.synchronize()
+        rms = []
+        for _ in range(args.restore_steps):
+            if scratch is not None:
+                scratch.fill_(0x33)
+            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            r0.record(stream)
+            lib.copy_regions(rest, rws.data_ptr(), rws.numel(), stream)
+            r1.record(stream)
+            torch.cuda.synchronize()
+            rms.append(r0.elapsed_time(r1))
+        # context: the runtime's own device-to-device copy of the whole arena
+        t0e, t1e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0e.record(stream)
+        backup.copy_(st.cand)
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        torch_copy_ms = t0e.elapsed_time(t1e)
+        st.diff(stream)
+        restored_ok = st.seg_results() == results
+        moved = sum(n for _, n in spans)
+        med_r = statistics.median(rms)
+        restore = {"ms_median": round(med_r, 4), "bytes_per_side": moved,
+                   "GBps_read_plus_write": round(2 * moved / (med_r * 1e-3) / 1e9, 2),
+                   "pct_of_hbm_peak": round(100 * 2 * moved / (med_r * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+                   "diff_after_restore_identical": restored_ok,
+                   "torch_copy_GBps_read_plus_write": round(2 * st.cand.numel() / (torch_copy_ms * 1e-3) / 1e9, 2)}
+        del backup, rws
+        torch.cuda.empty_cache()
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 3),
@@ -233,6 +274,7 @@ def main():
                      "traffic": pmc_traffic() if args.workload == "sweep" and not args.small else None,
                      "kernel": "diff_kernel (event span also holds the descriptor upload and result init)"},
         "diff_cosine": cosine,
+        "restore": restore,
         "total_mismatches": int(sum(r["mismatches"] for r in results)),
         "total_bitwise": int(sum(r["bitwise_mismatches"] for r in results)),
     }

@@ -284,6 +284,29 @@ asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t
                                  asmevo_guard_result* results,
                                  void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * One region of a captured pre-dispatch state (section 3.4, Tier 2: the
+ * dispatch's referenced device-memory regions and their pre-state are
+ * recorded once; every candidate replays with identical memory contents).
+ */
+typedef struct {
+  uint64_t dst, src;   /* device addresses */
+  uint64_t bytes;
+} asmevo_region;
+
+/*
+ * asmevo_copy_regions -- copies every region (dst <- src, `bytes` bytes) in
+ * one launch: a snapshot (live -> backup) or a restore (backup -> live) of a
+ * captured state, in place so that absolute device pointers inside the state
+ * stay valid.  Any alignment is accepted; regions whose source and
+ * destination share their address modulo 16 move in 16-byte chunks.
+ * Requirements: non-null addresses for non-empty regions; no destination
+ * range may overlap another destination or any source range.  Errors:
+ * ASMEVO_E_INVALID, ASMEVO_E_WORKSPACE (needs asmevo_workspace_bytes(n, 0)).
+ */
+asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n,
+                                  void* workspace, size_t ws_bytes, void* stream);
+
 /* Workspace bytes sufficient for any of the three calls with up to n_descs
  * descriptors and n_inj injections. */
 size_t asmevo_workspace_bytes(int32_t n_descs, int64_t n_inj);

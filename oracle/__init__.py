@@ -87,6 +87,10 @@ class RefCosResult(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class RefRegion(ctypes.Structure):
+    _fields_ = [("dst", ctypes.c_void_p), ("src", ctypes.c_void_p), ("bytes", ctypes.c_int64)]
+
+
 class RefGuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
                 ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
@@ -127,6 +131,7 @@ def lib() -> ctypes.CDLL:
         L.ref_cosine_segment.argtypes = [P(RefSeg), vp, vp, P(RefCosResult)]
         L.ref_pairwise_tree.argtypes = [vp, ctypes.c_int64]
         L.ref_pairwise_tree.restype = ctypes.c_double
+        L.ref_copy_regions.argtypes = [P(RefRegion), ctypes.c_int64]
         L.ref_guard_check.argtypes = [ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_int64,
                                       vp, ctypes.c_int64, P(RefGuardResult)]
         L.ref_decode_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, vp, vp]
@@ -328,6 +333,16 @@ def diff_workload(w, cand: np.ndarray, ref: np.ndarray, threads: int = 1) -> Lis
     from concurrent.futures import ThreadPoolExecutor
     with ThreadPoolExecutor(threads) as ex:
         return list(ex.map(one, w.compares))
+
+
+def copy_regions(buf: np.ndarray, regions) -> None:
+    """regions: (dst_offset, src_offset, bytes) inside the uint8 array `buf`, copied in order."""
+    arr = (RefRegion * max(1, len(regions)))()
+    base = _ptr(buf)
+    for k, (d, s_, n) in enumerate(regions):
+        assert 0 <= d and d + n <= buf.size and 0 <= s_ and s_ + n <= buf.size
+        arr[k] = RefRegion(base + d, base + s_, n)
+    lib().ref_copy_regions(arr, len(regions))
 
 
 def guard_check(seed: int, alloc_id: int, lo: np.ndarray, hi: np.ndarray) -> Dict:

@@ -662,6 +662,14 @@ int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, r
 }
 
 /* ------------------------------------------------------------------------ */
+/* Tier-2 state restore: plain byte copies.                                  */
+/* ------------------------------------------------------------------------ */
+void ref_copy_regions(const ref_region* regions, int64_t n) {
+  for (int64_t k = 0; k < n; ++k)
+    for (int64_t p = 0; p < regions[k].bytes; ++p) regions[k].dst[p] = regions[k].src[p];
+}
+
+/* ------------------------------------------------------------------------ */
 /* Guard check: every guard byte against the regenerated canary.             */
 /* ------------------------------------------------------------------------ */
 int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t n_lo,

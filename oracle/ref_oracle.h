@@ -116,6 +116,15 @@ int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, r
 /* the left-complete pairwise tree alone (exposed for its pins) */
 double ref_pairwise_tree(const double* x, int64_t n);
 
+/* Restore / snapshot of captured regions: dst[k][0..bytes) = src[k][0..bytes)
+ * for each region, in order (regions are host memory here). */
+typedef struct {
+  uint8_t* dst;
+  const uint8_t* src;
+  int64_t bytes;
+} ref_region;
+void ref_copy_regions(const ref_region* regions, int64_t n);
+
 /* bulk loops over the scalar functions above (used by the pin tests) */
 void ref_decode_n(int32_t dtype, const uint64_t* raw, int64_t n, int32_t* cls, double* value);
 void ref_encode_f32_n(int32_t dtype, const float* x, int64_t n, int saturate, uint64_t* out);

@@ -75,6 +75,10 @@ class CosineResult(ctypes.Structure):
                 ("cosine", ctypes.c_double), ("pairs", ctypes.c_uint64), ("blocks", ctypes.c_uint64)]
 
 
+class Region(ctypes.Structure):
+    _fields_ = [("dst", ctypes.c_uint64), ("src", ctypes.c_uint64), ("bytes", ctypes.c_uint64)]
+
+
 class GuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
                 ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
@@ -84,7 +88,7 @@ SEGMENT_RESULT_FIELDS = [f for f, _ in SegmentResult._fields_]
 GUARD_RESULT_FIELDS = [f for f, _ in GuardResult._fields_]
 
 EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments_ex",
-            "asmevo_diff_cosine", "asmevo_diff_cosine_workspace_bytes",
+            "asmevo_diff_cosine", "asmevo_diff_cosine_workspace_bytes", "asmevo_copy_regions",
             "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
             "asmevo_abi_version", "asmevo_last_hip_error"]
 
@@ -120,6 +124,8 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_diff_cosine.restype = ctypes.c_int32
         L.asmevo_diff_cosine_workspace_bytes.argtypes = [P(Segment), ctypes.c_int32]
         L.asmevo_diff_cosine_workspace_bytes.restype = ctypes.c_size_t
+        L.asmevo_copy_regions.argtypes = [P(Region), ctypes.c_int32, vp, ctypes.c_size_t, vp]
+        L.asmevo_copy_regions.restype = ctypes.c_int32
         L.asmevo_guard_check.argtypes = [P(Alloc), ctypes.c_int32, ctypes.c_uint64, vp, vp,
                                          ctypes.c_size_t, vp]
         L.asmevo_guard_check.restype = ctypes.c_int32
@@ -191,6 +197,12 @@ def diff_cosine(segments: Sequence[Segment], results_ptr: int, cos_results_ptr: 
     _check(_lib().asmevo_diff_cosine(s, len(segments), results_ptr, cos_results_ptr, workspace_ptr,
                                      workspace_size, _stream_handle(stream)),
            "asmevo_diff_cosine")
+
+
+def copy_regions(regions: Sequence[Region], workspace_ptr: int, workspace_size: int, stream=None) -> None:
+    r = _array(Region, regions)
+    _check(_lib().asmevo_copy_regions(r, len(regions), workspace_ptr, workspace_size, _stream_handle(stream)),
+           "asmevo_copy_regions")
 
 
 def guard_check(allocs: Sequence[Alloc], seed: int, results_ptr: int, workspace_ptr: int,

@@ -390,6 +390,57 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
 }
 
 // ---------------------------------------------------------------------------
+asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n, void* workspace,
+                                  size_t ws_bytes, void* stream) {
+  if (n < 0 || (n > 0 && !regions)) return ASMEVO_E_INVALID;
+  if (n == 0) return ASMEVO_OK;
+  std::vector<CopyRegion> dev((size_t)n);
+  std::vector<std::pair<uint64_t, uint64_t>> dsts, srcs;
+  uint64_t tiles = 0;
+  const uint64_t tile_bytes = (uint64_t)kTileChunks * kChunk;
+  for (int32_t k = 0; k < n; ++k) {
+    const asmevo_region& R = regions[k];
+    CopyRegion& C = dev[k];
+    std::memset(&C, 0, sizeof(C));
+    C.tile_begin = tiles;
+    if (R.bytes == 0) continue;
+    if (!R.dst || !R.src || R.bytes > (1ull << 52)) return ASMEVO_E_INVALID;
+    if (R.dst + R.bytes < R.dst || R.src + R.bytes < R.src) return ASMEVO_E_INVALID;
+    if (R.dst < R.src + R.bytes && R.src < R.dst + R.bytes) return ASMEVO_E_INVALID;   // memcpy semantics
+    dsts.emplace_back(R.dst, R.dst + R.bytes);
+    srcs.emplace_back(R.src, R.src + R.bytes);
+    C.dst = R.dst;
+    C.src = R.src;
+    C.bytes = R.bytes;
+    C.vec = (R.dst % kChunk) == (R.src % kChunk);
+    if (C.vec) {
+      const uint64_t head = (kChunk - R.src % kChunk) % kChunk;
+      C.head = head < R.bytes ? head : R.bytes;
+      C.body_bytes = R.bytes - C.head;
+      const uint64_t body_chunks = C.body_bytes / kChunk;
+      C.tile_count = std::max<uint64_t>(1, (body_chunks + kTileChunks - 1) / kTileChunks);
+    } else {
+      C.tile_count = (R.bytes + tile_bytes - 1) / tile_bytes;
+    }
+    tiles += C.tile_count;
+  }
+  // destinations pairwise disjoint, and disjoint from every source
+  std::sort(dsts.begin(), dsts.end());
+  for (size_t i = 1; i < dsts.size(); ++i)
+    if (dsts[i].first < dsts[i - 1].second) return ASMEVO_E_INVALID;
+  for (const auto& sr : srcs) {
+    auto it = std::lower_bound(dsts.begin(), dsts.end(), std::make_pair(sr.second, (uint64_t)0));
+    if (it != dsts.begin() && std::prev(it)->second > sr.first) return ASMEVO_E_INVALID;
+  }
+  const size_t bytes = dev.size() * sizeof(CopyRegion);
+  if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_copy(reinterpret_cast<const CopyRegion*>(workspace), n, tiles, device_cus() * 4, s));
+  return ASMEVO_OK;
+}
+
+// ---------------------------------------------------------------------------
 asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
                                  asmevo_guard_result* results, void* workspace, size_t ws_bytes,
                                  void* stream) {

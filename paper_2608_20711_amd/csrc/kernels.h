@@ -22,6 +22,9 @@ hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        double* partials = nullptr, unsigned long long* nonfinite_pairs = nullptr,
                        asmevo_cosine_result* cos_results = nullptr);
 
+hipError_t launch_copy(const CopyRegion* regs, int n, uint64_t total_tiles, int workgroups,
+                       hipStream_t stream);
+
 hipError_t launch_guard(const GuardRegion* regs, int n_regs, uint64_t total_chunks, uint64_t seed,
                         asmevo_guard_result* results, int n_results, hipStream_t stream);
 

@@ -81,6 +81,16 @@ struct PointEntry {             // one deduplicated point injection
 };
 static_assert(sizeof(PointEntry) == 40, "PointEntry layout");
 
+// ---------------------------------------------------------------- copy
+struct CopyRegion {             // 64 bytes
+  uint64_t dst, src, bytes;
+  uint64_t head;                // bytes before src/dst reach 16-byte alignment (vec regions)
+  uint64_t body_bytes;          // bytes - head; moved in whole 16-byte chunks, the rest by the last tile
+  uint64_t tile_begin, tile_count;
+  uint32_t vec, pad0;           // vec: src and dst have the same address phase modulo 16
+};
+static_assert(sizeof(CopyRegion) == 64, "CopyRegion layout");
+
 // ---------------------------------------------------------------- guard
 struct GuardRegion {            // one guard side of one allocation
   uint64_t addr;                // first guard byte

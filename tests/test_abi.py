@@ -38,7 +38,7 @@ def test_struct_layouts_match_header(tmp_path):
     fields = {
         "asmevo_alloc": lib.Alloc, "asmevo_injection": lib.Injection, "asmevo_segment": lib.Segment,
         "asmevo_segment_result": lib.SegmentResult, "asmevo_guard_result": lib.GuardResult,
-        "asmevo_cosine_result": lib.CosineResult,
+        "asmevo_cosine_result": lib.CosineResult, "asmevo_region": lib.Region,
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "asmevo.h"', "int main(void) {"]
     for cname, cls in fields.items():
@@ -179,3 +179,22 @@ def test_cosine_workspace_and_errors():
     with pytest.raises(lib.AsmevoError) as e:
         lib.diff_cosine([_seg()], 0x40000, 0, 0x50000, 1 << 20, stream=0)
     assert e.value.status == lib.E_INVALID
+
+
+@pytest.mark.parametrize("regions", [
+    [(0x1000, 0, 16)],                                   # null source
+    [(0x1000, 0x2000, 1 << 53)],                         # too large
+    [(0x1000, 0x1008, 64)],                              # source and destination overlap
+    [(0x1000, 0x9000, 64), (0x1020, 0xA000, 64)],        # destinations overlap
+    [(0x1000, 0x9000, 64), (0x9000, 0xB000, 64)],        # a destination overlaps another source
+])
+def test_copy_regions_argument_errors(regions):
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.copy_regions([lib.Region(d, s, n) for d, s, n in regions], 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+
+
+def test_copy_regions_workspace():
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.copy_regions([lib.Region(0x1000, 0x9000, 64)], 0x50000, 8, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
