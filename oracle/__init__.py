@@ -30,7 +30,7 @@ DTYPE = {"f32": 1, "bf16": 2, "f16": 3, "fp8e4m3": 4, "i32": 5, "i64": 6, "u8": 
 ESIZE = {1: 4, 2: 2, 3: 2, 4: 1, 5: 4, 6: 8, 7: 1}
 MODE = {"bitwise": 0, "tolerance": 1}
 NAN_POLICY = {"equal": 0, "strict": 1}
-DIST = {"normal": 0, "uniform_int": 1, "bits": 2, "const": 3}
+DIST = {"normal": 0, "uniform_int": 1, "bits": 2, "const": 3, "boundary": 4}
 KIND = {"flip_bit": 1, "step_within": 2, "set_beyond": 3, "set_nan": 4, "set_inf": 5,
         "guard_write_lo": 6, "guard_write_hi": 7}
 RATE = 0x100

@@ -312,6 +312,52 @@ static uint64_t esize_mask(int es) {
   return es == 8 ? ~(uint64_t)0 : (((uint64_t)1 << (8 * es)) - 1);
 }
 
+/* Boundary patterns per element type (16 each): signed zeros, the smallest
+ * and largest subnormals, the smallest normal, +-1 and the neighbours of 1,
+ * +-largest finite, +-Inf and NaNs (fp8 e4m3 has no Inf: NaN instead);
+ * for integers the extremes and alternating bit patterns. */
+static uint64_t boundary_pattern(int32_t dtype, uint32_t k) {
+  static const uint32_t f32[16] = {0x00000000u, 0x80000000u, 0x00000001u, 0x80000001u,
+                                   0x007FFFFFu, 0x00800000u, 0x3F800000u, 0xBF800000u,
+                                   0x3F7FFFFFu, 0x3F800001u, 0x7F7FFFFFu, 0xFF7FFFFFu,
+                                   0x7F800000u, 0xFF800000u, 0x7FC00000u, 0x7F800001u};
+  static const uint16_t bf16[16] = {0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x0080, 0x3F80, 0xBF80,
+                                    0x3F7F, 0x3F81, 0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x7FC0, 0x7F81};
+  static const uint16_t f16[16] = {0x0000, 0x8000, 0x0001, 0x8001, 0x03FF, 0x0400, 0x3C00, 0xBC00,
+                                   0x3BFF, 0x3C01, 0x7BFF, 0xFBFF, 0x7C00, 0xFC00, 0x7E00, 0x7C01};
+  static const uint8_t fp8[16] = {0x00, 0x80, 0x01, 0x81, 0x07, 0x08, 0x38, 0xB8,
+                                  0x37, 0x39, 0x7E, 0xFE, 0x7F, 0xFF, 0x7F, 0x7D};
+  static const uint32_t i32[16] = {0x00000000u, 0x00000001u, 0xFFFFFFFFu, 0x80000000u,
+                                   0x7FFFFFFFu, 0x80000001u, 0x7FFFFFFEu, 0x55555555u,
+                                   0xAAAAAAAAu, 0x000000FFu, 0x0000FFFFu, 0x00010000u,
+                                   0xFFFF0000u, 0x00000080u, 0x7F7F7F7Fu, 0x00000002u};
+  static const uint64_t i64[16] = {0x0ull, 0x1ull, 0xFFFFFFFFFFFFFFFFull, 0x8000000000000000ull,
+                                   0x7FFFFFFFFFFFFFFFull, 0x8000000000000001ull, 0x7FFFFFFFFFFFFFFEull,
+                                   0x5555555555555555ull, 0xAAAAAAAAAAAAAAAAull, 0xFFull, 0xFFFFFFFFull,
+                                   0x100000000ull, 0xFFFFFFFF00000000ull, 0x80000000ull, 0x7FFFFFFFull,
+                                   0x2ull};
+  static const uint8_t u8[16] = {0x00, 0x01, 0xFF, 0x80, 0x7F, 0x81, 0x7E, 0x55,
+                                 0xAA, 0x0F, 0xF0, 0x10, 0xEF, 0x40, 0xBF, 0x02};
+  k &= 15u;
+  switch (dtype) {
+    case REF_F32: return f32[k];
+    case REF_BF16: return bf16[k];
+    case REF_F16: return f16[k];
+    case REF_FP8E4M3: return fp8[k];
+    case REF_I32: return i32[k];
+    case REF_I64: return i64[k];
+    default: return u8[k];
+  }
+}
+
+/* BOUNDARY threshold: element is a boundary pattern iff its draw is below
+ * floor(rate * 2^32 + 1/2), the rate clamped to [0, 1]. */
+static uint64_t boundary_threshold(double rate) {
+  if (!(rate > 0.0)) return 0;
+  if (rate >= 1.0) return (uint64_t)1 << 32;
+  return (uint64_t)floor(rate * 4294967296.0 + 0.5);
+}
+
 static uint64_t base_element(const ref_alloc* A, uint64_t seed, int64_t i) {
   int es = ref_esize(A->dtype);
   uint32_t X[4];
@@ -337,6 +383,18 @@ static uint64_t base_element(const ref_alloc* A, uint64_t seed, int64_t i) {
       bits |= (uint64_t)stream_byte(seed, A->alloc_id, PURPOSE_VALUE, 0, 0, q) << (8 * k);
     }
     return bits;
+  }
+  if (A->dist == REF_BOUNDARY) {
+    /* one VALUE block per element: x selects, y picks the pattern, (z, w)
+     * give a Box-Muller cosine value of standard deviation p1 otherwise */
+    stream_block(seed, A->alloc_id, PURPOSE_VALUE, 0, 0, (uint64_t)i, X);
+    if ((uint64_t)X[0] < boundary_threshold(A->p0)) return boundary_pattern(A->dtype, X[1]);
+    if (is_float(A->dtype)) {
+      double z = ref_normal(X[2], X[3], 0);
+      double v = A->p1 * z;
+      return ref_encode_f32(A->dtype, (float)v, A->saturate);
+    }
+    return ((uint64_t)X[2] | ((uint64_t)X[3] << 32)) & esize_mask(es);
   }
   /* REF_CONST */
   if (is_float(A->dtype)) return ref_encode_f32(A->dtype, (float)A->p0, A->saturate);

@@ -23,7 +23,7 @@ enum { REF_F32 = 1, REF_BF16 = 2, REF_F16 = 3, REF_FP8E4M3 = 4, REF_I32 = 5, REF
 enum { REF_BITWISE = 0, REF_TOLERANCE = 1 };
 enum { REF_NAN_EQUAL = 0, REF_NAN_STRICT = 1 };
 /* value distributions of a fill */
-enum { REF_NORMAL = 0, REF_UNIFORM_INT = 1, REF_BITS = 2, REF_CONST = 3 };
+enum { REF_NORMAL = 0, REF_UNIFORM_INT = 1, REF_BITS = 2, REF_CONST = 3, REF_BOUNDARY = 4 };
 /* injection kinds; REF_RATE is or-ed into the kind of a Bernoulli rule */
 enum {
   REF_FLIP_BIT = 1, REF_STEP_WITHIN = 2, REF_SET_BEYOND = 3, REF_SET_NAN = 4, REF_SET_INF = 5,
@@ -39,7 +39,7 @@ typedef struct {
   int64_t guard_lo, guard_hi;   /* bytes */
   int32_t dist;
   int32_t saturate;        /* fp8: clamp to +-448 before rounding */
-  double p0, p1;           /* NORMAL mean/std; CONST value */
+  double p0, p1;           /* NORMAL mean/std; CONST value; BOUNDARY rate/std */
   int64_t i0, i1;          /* UNIFORM_INT [i0, i1); CONST integer value */
 } ref_alloc;
 

@@ -56,9 +56,9 @@ class Alloc:
     stride: int
     guard_lo: int = 0
     guard_hi: int = 0
-    dist: str = "normal"          # normal | uniform_int | bits | const
-    p0: float = 0.0               # normal: mean; const: value
-    p1: float = 1.0               # normal: standard deviation
+    dist: str = "normal"          # normal | uniform_int | bits | const | boundary
+    p0: float = 0.0               # normal: mean; const: value; boundary: rate of boundary patterns
+    p1: float = 1.0               # normal, boundary: standard deviation
     i0: int = 0                   # uniform_int: [i0, i1)
     i1: int = 0
     saturate: bool = False        # fp8: clamp to +-448 before rounding
