@@ -91,8 +91,29 @@ enum {
   ASMEVO_DIST_NORMAL = 0,       /* N(p0, p1^2): Box-Muller, then fp32 (RNE), then dtype (RNE) */
   ASMEVO_DIST_UNIFORM_INT = 1,  /* integers uniform in [i0, i1), 0 < i1 - i0 <= 2^32 */
   ASMEVO_DIST_BITS = 2,         /* raw generator bytes */
-  ASMEVO_DIST_CONST = 3         /* p0 (float dtypes, via fp32) or i0 (integer dtypes) */
+  ASMEVO_DIST_CONST = 3,        /* p0 (float dtypes, via fp32) or i0 (integer dtypes) */
+  ASMEVO_DIST_BOUNDARY = 4      /* boundary values at rate p0 (0 <= p0 <= 1), else N(0, p1^2)
+                                   (float dtypes) or raw generator bits (integer dtypes); below */
 };
+
+/*
+ * ASMEVO_DIST_BOUNDARY (section 3.4, Tier 1: inputs that cover boundary
+ * values).  Element i draws one VALUE block (x, y, z, w).  If x < T, with
+ * T = 2^32 for p0 = 1 and floor(p0 * 2^32 + 1/2) otherwise, the element is
+ * boundary pattern (y mod 16) of its type; otherwise it is p1 * rho * cos
+ * from the Box-Muller pair (z, w), rounded to fp32 and then to the dtype
+ * (float dtypes), or the bits of z | w << 32 (integer dtypes).
+ * Float patterns 0..15: +0, -0, +min subnormal, -min subnormal, max
+ * subnormal, min normal, +1, -1, the float below 1, the float above 1, +max
+ * finite, -max finite, +Inf, -Inf, quiet NaN (the canonical one), signalling
+ * NaN (payload 1).  fp8 e4m3 has no infinities and one NaN per sign: 12 and
+ * 14 are 0x7F, 13 is 0xFF, 15 is the largest finite below max (0x7D).
+ * Integer patterns (s = the sign bit, m = all ones of the width): 0, 1, m,
+ * s, m^s, s|1, (m^s)-1, 0x55.., 0xAA.., then per width
+ *   u8:  0x0F, 0xF0, 0x10, 0xEF, 0x40, 0xBF, 2
+ *   i32: 0xFF, 0xFFFF, 0x10000, 0xFFFF0000, 0x80, 0x7F7F7F7F, 2
+ *   i64: 0xFF, 0xFFFFFFFF, 2^32, 0xFFFFFFFF00000000, 0x80000000, 0x7FFFFFFF, 2.
+ */
 #define ASMEVO_FILL_SATURATE 1u  /* fp8: clamp to +-448 before rounding */
 
 /*

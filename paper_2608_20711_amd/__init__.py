@@ -22,7 +22,7 @@ OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, -1, -2, -3, -4
 F32, BF16, F16, FP8_E4M3, I32, I64, U8 = 1, 2, 3, 4, 5, 6, 7
 BITWISE, TOLERANCE = 0, 1
 NAN_EQUAL, NAN_STRICT = 0, 1
-DIST_NORMAL, DIST_UNIFORM_INT, DIST_BITS, DIST_CONST = 0, 1, 2, 3
+DIST_NORMAL, DIST_UNIFORM_INT, DIST_BITS, DIST_CONST, DIST_BOUNDARY = 0, 1, 2, 3, 4
 FILL_SATURATE = 1
 INJ_FLIP_BIT, INJ_STEP_WITHIN, INJ_SET_BEYOND, INJ_SET_NAN, INJ_SET_INF = 1, 2, 3, 4, 5
 INJ_GUARD_WRITE_LO, INJ_GUARD_WRITE_HI = 6, 7
@@ -32,7 +32,8 @@ SIDE_CANDIDATE, SIDE_BOTH = 0, 1
 DTYPE_CODE = {"f32": F32, "bf16": BF16, "f16": F16, "fp8e4m3": FP8_E4M3, "i32": I32, "i64": I64, "u8": U8}
 MODE_CODE = {"bitwise": BITWISE, "tolerance": TOLERANCE}
 NAN_CODE = {"equal": NAN_EQUAL, "strict": NAN_STRICT}
-DIST_CODE = {"normal": DIST_NORMAL, "uniform_int": DIST_UNIFORM_INT, "bits": DIST_BITS, "const": DIST_CONST}
+DIST_CODE = {"normal": DIST_NORMAL, "uniform_int": DIST_UNIFORM_INT, "bits": DIST_BITS, "const": DIST_CONST,
+             "boundary": DIST_BOUNDARY}
 KIND_CODE = {"flip_bit": INJ_FLIP_BIT, "step_within": INJ_STEP_WITHIN, "set_beyond": INJ_SET_BEYOND,
              "set_nan": INJ_SET_NAN, "set_inf": INJ_SET_INF, "guard_write_lo": INJ_GUARD_WRITE_LO,
              "guard_write_hi": INJ_GUARD_WRITE_HI}

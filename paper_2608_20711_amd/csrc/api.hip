@@ -138,6 +138,10 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
       case ASMEVO_DIST_CONST:
         if (is_float(A.dtype) && !std::isfinite(A.p0)) return ASMEVO_E_INVALID;
         break;
+      case ASMEVO_DIST_BOUNDARY:
+        if (!(A.p0 >= 0.0 && A.p0 <= 1.0) || (is_float(A.dtype) && !std::isfinite(A.p1)))
+          return ASMEVO_E_INVALID;
+        break;
       default:
         return ASMEVO_E_INVALID;
     }
@@ -155,6 +159,8 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
     F.p1 = A.p1;
     F.i0 = A.i0;
     F.i1 = A.i1;
+    if (A.dist == ASMEVO_DIST_BOUNDARY)   // selection threshold on a 32-bit draw
+      F.i0 = A.p0 >= 1.0 ? (int64_t)(1ll << 32) : (int64_t)std::floor(A.p0 * 4294967296.0 + 0.5);
     F.dtype = A.dtype;
     F.esize = (uint32_t)es;
     F.alloc_id = A.alloc_id;

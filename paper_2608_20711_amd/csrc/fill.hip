@@ -27,6 +27,73 @@ __device__ __forceinline__ uint64_t emask(uint32_t es) {
   return es == 8 ? ~0ull : ((1ull << (8u * es)) - 1ull);
 }
 
+// Boundary pattern k (0..15) of an element type.  Float patterns come from
+// the format's exponent and mantissa widths; integer patterns from the width.
+__device__ __forceinline__ uint64_t boundary_bits(uint32_t dtype, uint32_t es, uint32_t k) {
+  const uint32_t W = 8u * es;
+  const uint64_t mask = emask(es);
+  const uint64_t sign = 1ull << (W - 1u);
+  if (dtype <= ASMEVO_FP8_E4M3) {
+    const uint32_t M = dtype == ASMEVO_F32 ? 23u : dtype == ASMEVO_BF16 ? 7u : dtype == ASMEVO_F16 ? 10u : 3u;
+    const uint32_t E = W - 1u - M;
+    const uint64_t one = ((1ull << (E - 1u)) - 1ull) << M;   // biased exponent of 1.0
+    const uint64_t expo = ((1ull << E) - 1ull) << M;         // all-ones exponent field
+    const bool fp8 = dtype == ASMEVO_FP8_E4M3;
+    const uint64_t maxf = fp8 ? 0x7Eull : expo - 1ull;
+    switch (k) {
+      case 0: return 0;
+      case 1: return sign;
+      case 2: return 1;
+      case 3: return sign | 1ull;
+      case 4: return (1ull << M) - 1ull;
+      case 5: return 1ull << M;
+      case 6: return one;
+      case 7: return sign | one;
+      case 8: return one - 1ull;
+      case 9: return one + 1ull;
+      case 10: return maxf;
+      case 11: return sign | maxf;
+      case 12: return fp8 ? 0x7Full : expo;
+      case 13: return fp8 ? 0xFFull : sign | expo;
+      case 14: return fp8 ? 0x7Full : expo | (1ull << (M - 1u));
+      default: return fp8 ? maxf - 1ull : expo | 1ull;
+    }
+  }
+  switch (k) {
+    case 0: return 0;
+    case 1: return 1;
+    case 2: return mask;
+    case 3: return sign;
+    case 4: return mask ^ sign;
+    case 5: return sign | 1ull;
+    case 6: return (mask ^ sign) - 1ull;
+    case 7: return 0x5555555555555555ull & mask;
+    case 8: return 0xAAAAAAAAAAAAAAAAull & mask;
+    default: break;
+  }
+  if (es == 1) {
+    switch (k) {
+      case 9: return 0x0F;
+      case 10: return 0xF0;
+      case 11: return 0x10;
+      case 12: return 0xEF;
+      case 13: return 0x40;
+      case 14: return 0xBF;
+      default: return 2;
+    }
+  }
+  const uint32_t H = W / 2u;                                   // half width
+  switch (k) {
+    case 9: return 0xFF;
+    case 10: return (1ull << H) - 1ull;
+    case 11: return 1ull << H;
+    case 12: return mask ^ ((1ull << H) - 1ull);
+    case 13: return es == 4 ? 0x80ull : 0x80000000ull;
+    case 14: return es == 4 ? 0x7F7F7F7Full : 0x7FFFFFFFull;
+    default: return 2;
+  }
+}
+
 // Base value of element i (before any injection), for an element whose
 // generator block has already been drawn: X = VALUE block i/4.
 __device__ __forceinline__ uint64_t base_from_block(const FillAlloc& A, const U4& X, uint64_t i,
@@ -56,6 +123,18 @@ __device__ __forceinline__ uint64_t base_from_block(const FillAlloc& A, const U4
       for (uint32_t k = 0; k < A.esize; ++k)
         bits |= (uint64_t)byte_of(B, (uint32_t)((q0 + k) & 15u)) << (8u * k);
       return bits;
+    }
+    case ASMEVO_DIST_BOUNDARY: {
+      // its own VALUE block i: x selects (threshold in i0), y picks the pattern
+      const U4 B = stream(seed, A.alloc_id, kValue, 0, 0, i);
+      if ((uint64_t)B.x < (uint64_t)A.i0) return boundary_bits(A.dtype, A.esize, B.y & 15u);
+      if (A.dtype <= ASMEVO_FP8_E4M3) {
+        double z0, z1;
+        box_muller(B.z, B.w, z0, z1);
+        const double v = A.p1 * z0;
+        return encode_f32(A.dtype, (float)v, A.saturate != 0);
+      }
+      return ((uint64_t)B.z | ((uint64_t)B.w << 32)) & emask(A.esize);
     }
     default:  // CONST
       if (A.dtype <= ASMEVO_FP8_E4M3) return encode_f32(A.dtype, (float)A.p0, A.saturate != 0);
