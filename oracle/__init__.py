@@ -32,7 +32,7 @@ MODE = {"bitwise": 0, "tolerance": 1}
 NAN_POLICY = {"equal": 0, "strict": 1}
 DIST = {"normal": 0, "uniform_int": 1, "bits": 2, "const": 3, "boundary": 4}
 KIND = {"flip_bit": 1, "step_within": 2, "set_beyond": 3, "set_nan": 4, "set_inf": 5,
-        "guard_write_lo": 6, "guard_write_hi": 7}
+        "guard_write_lo": 6, "guard_write_hi": 7, "pad_write": 8}
 RATE = 0x100
 SIDES = {"candidate": 0, "both": 1}
 
@@ -93,7 +93,8 @@ class RefRegion(ctypes.Structure):
 
 class RefGuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
-                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
+                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64),
+                ("bad_pad", ctypes.c_uint64), ("first_bad_pad", ctypes.c_int64)]
 
     def as_dict(self) -> Dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -134,6 +135,7 @@ def lib() -> ctypes.CDLL:
         L.ref_copy_regions.argtypes = [P(RefRegion), ctypes.c_int64]
         L.ref_guard_check.argtypes = [ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_int64,
                                       vp, ctypes.c_int64, P(RefGuardResult)]
+        L.ref_pad_check.argtypes = [P(RefAlloc), ctypes.c_uint64, vp, P(RefGuardResult)]
         L.ref_decode_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, vp, vp]
         L.ref_encode_f32_n.argtypes = [ctypes.c_int32, vp, ctypes.c_int64, ctypes.c_int, vp]
         L.ref_log_u_n.argtypes = [vp, ctypes.c_int64, vp]
@@ -354,12 +356,28 @@ def guard_check(seed: int, alloc_id: int, lo: np.ndarray, hi: np.ndarray) -> Dic
     return res.as_dict()
 
 
+def pad_check(w, k: int, data: np.ndarray) -> Dict:
+    """Row-pad check of allocation k of workload w; `data` is its data region."""
+    data = np.ascontiguousarray(data, dtype=np.uint8)
+    assert data.size == w.allocs[k].data_bytes
+    res = RefGuardResult()
+    allocs = ref_allocs(w)
+    rc = lib().ref_pad_check(ctypes.byref(allocs[k]), w.seed, _ptr(data) if data.size else None,
+                             ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle pad check rejected the allocation")
+    return {"bad_pad": res.bad_pad, "first_bad_pad": res.first_bad_pad}
+
+
 def guard_workload(w, arena: np.ndarray) -> List[Dict]:
+    """Guard and row-pad check of every allocation of w in `arena`."""
     out = []
     for k, a in enumerate(w.allocs):
         o = w.offsets[k]
         lo = arena[o:o + a.guard_lo]
         h0 = o + a.guard_lo + a.data_bytes
         hi = arena[h0:h0 + a.guard_hi]
-        out.append(guard_check(w.seed, a.alloc_id, lo, hi))
+        r = guard_check(w.seed, a.alloc_id, lo, hi)
+        r.update(pad_check(w, k, arena[o + a.guard_lo:h0]))
+        out.append(r)
     return out

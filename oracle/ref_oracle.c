@@ -484,7 +484,7 @@ uint64_t ref_element(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int
     const ref_inj* J = &inj[t];
     if (J->alloc != (uint32_t)k || (J->kind & REF_RATE)) continue;
     uint32_t kind = J->kind & 0xFFu;
-    if (kind == REF_GUARD_WRITE_LO || kind == REF_GUARD_WRITE_HI) continue;
+    if (kind == REF_GUARD_WRITE_LO || kind == REF_GUARD_WRITE_HI || kind == REF_PAD_WRITE) continue;
     if (J->index != i || !applies(J, variant)) continue;
     uint32_t vsel = (J->sides == REF_SIDE_BOTH) ? 0 : variant;
     value = apply_injection(A, J, base, seed, vsel, i);
@@ -507,6 +507,18 @@ static int guard_written(const ref_inj* inj, int64_t n_inj, int32_t k, uint32_t 
     int s = (kind == REF_GUARD_WRITE_LO) ? 0 : (kind == REF_GUARD_WRITE_HI) ? 1 : -1;
     if (s != side || !applies(J, variant)) continue;
     if (p >= J->index && p < J->index + (int64_t)J->arg) hit = 1;
+  }
+  return hit;
+}
+
+/* Is data byte q of allocation k (a pad byte) inverted by a PAD_WRITE entry? */
+static int pad_written(const ref_inj* inj, int64_t n_inj, int32_t k, uint32_t variant, int64_t q) {
+  int hit = 0;
+  for (int64_t t = 0; t < n_inj; ++t) {
+    const ref_inj* J = &inj[t];
+    if (J->alloc != (uint32_t)k || (J->kind & REF_RATE) || (J->kind & 0xFFu) != REF_PAD_WRITE) continue;
+    if (!applies(J, variant)) continue;
+    if (q >= J->index && q < J->index + (int64_t)J->arg) hit = 1;
   }
   return hit;
 }
@@ -541,6 +553,7 @@ int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64
         byte = (uint8_t)(cached_bits >> (8 * (q % es)));
       } else {
         byte = stream_byte(seed, A->alloc_id, PURPOSE_PAD, 0, 0, (uint64_t)q);
+        if (pad_written(inj, n_inj, k, variant, q)) byte = (uint8_t)~byte;
       }
     } else {
       int64_t ph = p - A->guard_lo - D;
@@ -736,6 +749,8 @@ int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t
   res->bad_hi = 0;
   res->first_bad_lo = -1;
   res->first_bad_hi = -1;
+  res->bad_pad = 0;
+  res->first_bad_pad = -1;
   for (int64_t p = 0; p < n_lo; ++p) {
     if (lo[p] != ref_canary_byte(seed, alloc_id, 0, p)) {
       res->bad_lo += 1;
@@ -746,6 +761,24 @@ int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t
     if (hi[p] != ref_canary_byte(seed, alloc_id, 1, p)) {
       res->bad_hi += 1;
       if (res->first_bad_hi < 0) res->first_bad_hi = p;
+    }
+  }
+  return 0;
+}
+
+int ref_pad_check(const ref_alloc* A, uint64_t seed, const uint8_t* data, ref_guard_result* res) {
+  res->bad_pad = 0;
+  res->first_bad_pad = -1;
+  if (A->rows < 2 || A->stride <= A->cols) return 0;
+  int es = ref_esize(A->dtype);
+  if (es == 0) return -1;
+  int64_t D = data_bytes(A);
+  for (int64_t q = 0; q < D; ++q) {
+    int64_t e = q / es;
+    if (e % A->stride < A->cols) continue;        /* a data element, not padding */
+    if (data[q] != stream_byte(seed, A->alloc_id, PURPOSE_PAD, 0, 0, (uint64_t)q)) {
+      res->bad_pad += 1;
+      if (res->first_bad_pad < 0) res->first_bad_pad = q;
     }
   }
   return 0;

@@ -27,7 +27,8 @@ enum { REF_NORMAL = 0, REF_UNIFORM_INT = 1, REF_BITS = 2, REF_CONST = 3, REF_BOU
 /* injection kinds; REF_RATE is or-ed into the kind of a Bernoulli rule */
 enum {
   REF_FLIP_BIT = 1, REF_STEP_WITHIN = 2, REF_SET_BEYOND = 3, REF_SET_NAN = 4, REF_SET_INF = 5,
-  REF_GUARD_WRITE_LO = 6, REF_GUARD_WRITE_HI = 7
+  REF_GUARD_WRITE_LO = 6, REF_GUARD_WRITE_HI = 7,
+  REF_PAD_WRITE = 8        /* invert `arg` row-pad bytes from data byte offset `index` */
 };
 #define REF_RATE 0x100u
 enum { REF_SIDE_CANDIDATE = 0, REF_SIDE_BOTH = 1 };
@@ -47,8 +48,9 @@ typedef struct {
   uint32_t alloc;          /* index into the allocation array */
   uint32_t kind;           /* REF_* kind, optionally | REF_RATE */
   uint32_t sides;          /* REF_SIDE_* */
-  uint32_t arg;            /* bit index (0xffffffff = random) / Inf sign / guard byte count */
-  int64_t index;           /* element index, guard byte offset, or (RATE) threshold T */
+  uint32_t arg;            /* bit index (0xffffffff = random) / Inf sign / guard or pad byte count */
+  int64_t index;           /* element index, guard byte offset, data byte offset (PAD_WRITE),
+                              or (RATE) threshold T */
   double atol, rtol;       /* tolerance targeted by SET_BEYOND */
 } ref_inj;
 
@@ -70,6 +72,8 @@ typedef struct {
 typedef struct {
   uint64_t bad_lo, bad_hi;
   int64_t first_bad_lo, first_bad_hi;
+  uint64_t bad_pad;          /* row-pad bytes that differ from their canary */
+  int64_t first_bad_pad;     /* lowest such byte, as an offset from the first data byte */
 } ref_guard_result;
 
 /* Philox4x32-10 block function (Salmon et al., SC'11). */
@@ -98,9 +102,16 @@ int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64
 /* Compares one segment: a, b point at element (0,0) of candidate and reference. */
 int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res);
 
-/* Guard check of one allocation: lo/hi point at the first byte of each guard (may be NULL if 0). */
+/* Guard check of one allocation: lo/hi point at the first byte of each guard (may be NULL if 0).
+ * Sets bad_pad = 0 and first_bad_pad = -1. */
 int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t n_lo,
                     const uint8_t* hi, int64_t n_hi, ref_guard_result* res);
+
+/* Row-pad check of one allocation: `data` points at its first data byte; every
+ * byte of a row's padding (elements cols..stride-1 of rows 0..rows-2) is
+ * compared with the PAD byte the fill writes there.  Sets bad_pad and
+ * first_bad_pad of `res` only. */
+int ref_pad_check(const ref_alloc* A, uint64_t seed, const uint8_t* data, ref_guard_result* res);
 
 /* Cosine term of Eq. 1 over one segment (float dtypes).  sum_* are fp64
  * sums over the pairs with both values finite, in the defined order: rows

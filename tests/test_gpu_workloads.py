@@ -15,6 +15,9 @@ import torch
 import oracle
 import workloads
 from gpu_helpers import (THREADS, assert_fill_equal, assert_results_equal, check_fill_sampled, log,
+
+INTACT = {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1, "bad_pad": 0,
+          "first_bad_pad": -1}
                          run_gpu)
 
 pytestmark = pytest.mark.gpu
@@ -68,7 +71,7 @@ def test_sweep_full_size_sampled():
     st = run_gpu(w)
     res = st.seg_results()
     guards = st.guard_results()
-    assert all(g == {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1} for g in guards)
+    assert all(g == INTACT for g in guards)
     n_el = sum(a.n_elements for a in w.allocs)
     total_bw = sum(r["bitwise_mismatches"] for r in res)
     assert abs(total_bw - 1e-6 * n_el) < 6 * math.sqrt(1e-6 * n_el)

@@ -272,7 +272,7 @@ def test_guard_check_every_byte_of_tiny_guards():
     lo = np.array([oracle.canary_byte(seed, aid, 0, p) for p in range(n)], dtype=np.uint8)
     hi = np.array([oracle.canary_byte(seed, aid, 1, p) for p in range(n)], dtype=np.uint8)
     assert oracle.guard_check(seed, aid, lo, hi) == {"bad_lo": 0, "bad_hi": 0,
-                                                     "first_bad_lo": -1, "first_bad_hi": -1}
+                                                     "first_bad_lo": -1, "first_bad_hi": -1, "bad_pad": 0, "first_bad_pad": -1}
     assert not np.array_equal(lo, hi)          # the two sides carry different canaries
     for p in range(n):
         for side in (0, 1):
@@ -280,9 +280,9 @@ def test_guard_check_every_byte_of_tiny_guards():
             (l2 if side == 0 else h2)[p] ^= 0x40
             r = oracle.guard_check(seed, aid, l2, h2)
             if side == 0:
-                assert r == {"bad_lo": 1, "bad_hi": 0, "first_bad_lo": p, "first_bad_hi": -1}
+                assert r == {"bad_lo": 1, "bad_hi": 0, "first_bad_lo": p, "first_bad_hi": -1, "bad_pad": 0, "first_bad_pad": -1}
             else:
-                assert r == {"bad_lo": 0, "bad_hi": 1, "first_bad_lo": -1, "first_bad_hi": p}
+                assert r == {"bad_lo": 0, "bad_hi": 1, "first_bad_lo": -1, "first_bad_hi": p, "bad_pad": 0, "first_bad_pad": -1}
     # another seed or buffer id gives other canaries
     assert oracle.guard_check(seed + 1, aid, lo, hi)["bad_lo"] > n // 2
     assert oracle.guard_check(seed, aid + 1, lo, hi)["bad_lo"] > n // 2

@@ -17,6 +17,10 @@ import oracle
 import workloads
 from workloads import Alloc, Compare, Injection, Workload
 
+FLOAT = ("f32", "bf16", "f16", "fp8e4m3")
+INTACT = {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1, "bad_pad": 0,
+          "first_bad_pad": -1}
+
 
 def _values(dtype, raw_bytes):
     """fp64 values of a little-endian byte array via numpy / torch casts."""
@@ -132,8 +136,8 @@ def test_guards_intact_after_fill_and_guard_writes_detected():
     cand = P.fill_arena(1)
     g_ref = oracle.guard_workload(w, ref)[0]
     g_cand = oracle.guard_workload(w, cand)[0]
-    assert g_ref == {"bad_lo": 0, "bad_hi": 2, "first_bad_lo": -1, "first_bad_hi": 10}
-    assert g_cand == {"bad_lo": 3, "bad_hi": 3, "first_bad_lo": 5, "first_bad_hi": 10}
+    assert g_ref == {"bad_lo": 0, "bad_hi": 2, "first_bad_lo": -1, "first_bad_hi": 10, "bad_pad": 0, "first_bad_pad": -1}
+    assert g_cand == {"bad_lo": 3, "bad_hi": 3, "first_bad_lo": 5, "first_bad_hi": 10, "bad_pad": 0, "first_bad_pad": -1}
     # data untouched by guard writes
     assert np.array_equal(_data(w, ref, 0), _data(w, cand, 0))
 
@@ -289,7 +293,7 @@ def test_closed_form_int_lowp():
 def test_closed_form_sweep_small():
     w = workloads.sweep(small=True)
     P, ref, cand, res, guards = _run(w)
-    assert all(g == {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1} for g in guards)
+    assert all(g == INTACT for g in guards)
     total_bw = 0
     for k, r in enumerate(res):
         lc = _logical(w, cand, k)
@@ -305,3 +309,56 @@ def test_closed_form_sweep_small():
         total_bw += diff_el.size
     n_el = sum(a.n_elements for a in w.allocs)
     assert abs(total_bw - 1e-6 * n_el) < 5 * math.sqrt(n_el * 1e-6) + 3
+
+
+# ------------------------------------------------------------ row-pad canaries
+def _pad_mask(a):
+    """Data-region bytes that are row padding: element (q // es) has column >= cols."""
+    q = np.arange(a.data_bytes)
+    return (q // a.esize) % a.stride >= a.cols
+
+
+@pytest.mark.parametrize("dtype,rows,cols,stride", [("f32", 5, 7, 10), ("bf16", 4, 13, 16), ("u8", 6, 5, 9),
+                                                    ("i64", 3, 2, 5), ("f16", 1, 9, 12), ("fp8e4m3", 4, 8, 8)])
+def test_pad_check_flags_exactly_the_pad_bytes(dtype, rows, cols, stride):
+    """Brute force: invert each data-region byte in turn; the pad check counts it
+    iff numpy's pad mask says it is padding."""
+    a = Alloc(6, dtype, rows, cols, stride, 16, 16, "normal" if dtype in FLOAT else "bits")
+    w = Workload("t", "", 0x9AD, [a], [], [])
+    arena = oracle.Prepared(w).fill_arena(0)
+    o = w.data_offset(0)
+    data = arena[o:o + a.data_bytes].copy()
+    assert oracle.pad_check(w, 0, data) == {"bad_pad": 0, "first_bad_pad": -1}
+    mask = _pad_mask(a)
+    for q in range(a.data_bytes):
+        d2 = data.copy()
+        d2[q] ^= 0xFF
+        r = oracle.pad_check(w, 0, d2)
+        assert r == ({"bad_pad": 1, "first_bad_pad": q} if mask[q] else {"bad_pad": 0, "first_bad_pad": -1})
+    # a different seed's pads do not pass
+    w2 = Workload("t", "", 0x9AE, [a], [], [])
+    if mask.sum() >= 8:
+        assert oracle.pad_check(w2, 0, data)["bad_pad"] >= mask.sum() // 2
+
+
+def test_pad_write_injection():
+    a = Alloc(8, "bf16", 9, 30, 37, 32, 32, "normal", 0.0, 4.0)
+    es = a.esize
+    pitch = a.stride * es
+    # row 2: bytes 3..8 of its padding; row 7: the last pad byte of the row
+    inj = [Injection(0, "pad_write", arg=6, index=2 * pitch + a.cols * es + 3),
+           Injection(0, "pad_write", sides="both", arg=1, index=7 * pitch + pitch - 1)]
+    w = Workload("t", "", 0x51, [a], inj, [])
+    P = oracle.Prepared(w)
+    ref, cand = P.fill_arena(0), P.fill_arena(1)
+    g_ref = oracle.guard_workload(w, ref)[0]
+    g_cand = oracle.guard_workload(w, cand)[0]
+    assert g_ref["bad_pad"] == 1 and g_ref["first_bad_pad"] == 7 * pitch + pitch - 1
+    assert g_cand["bad_pad"] == 7 and g_cand["first_bad_pad"] == 2 * pitch + a.cols * es + 3
+    assert g_cand["bad_lo"] == 0 and g_cand["bad_hi"] == 0
+    # the written bytes are the complement of the reference's pad bytes; elements untouched
+    o = w.data_offset(0)
+    x = ref[o:o + a.data_bytes] ^ cand[o:o + a.data_bytes]
+    assert np.flatnonzero(x).tolist() == list(range(2 * pitch + a.cols * es + 3, 2 * pitch + a.cols * es + 9))
+    assert set(x[x != 0].tolist()) == {0xFF}
+    assert np.array_equal(_logical(w, ref, 0), _logical(w, cand, 0))
