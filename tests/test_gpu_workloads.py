@@ -15,10 +15,10 @@ import torch
 import oracle
 import workloads
 from gpu_helpers import (THREADS, assert_fill_equal, assert_results_equal, check_fill_sampled, log,
+                         run_gpu)
 
 INTACT = {"bad_lo": 0, "bad_hi": 0, "first_bad_lo": -1, "first_bad_hi": -1, "bad_pad": 0,
           "first_bad_pad": -1}
-                         run_gpu)
 
 pytestmark = pytest.mark.gpu
 
