@@ -16,8 +16,9 @@
  *   asmevo_diff_segments  element-wise compare of many buffers in one launch,
  *                         per-buffer counts / first index / max abs / max rel
  *                                                          (sec. 3.2, Eq. 1)
- *   asmevo_guard_check    canary integrity of every guard region  (sec. 3.2
- *                         iota, sec. 3.4)
+ *   asmevo_guard_check    canary integrity of every guard region and of
+ *                         the row padding                 (sec. 3.2 iota,
+ *                                                          sec. 3.4)
  *
  * Conventions for every call:
  *  - All addresses inside descriptors and all result pointers are HIP device
@@ -52,7 +53,7 @@
 extern "C" {
 #endif
 
-#define ASMEVO_ABI_VERSION 1
+#define ASMEVO_ABI_VERSION 2
 
 typedef int32_t asmevo_status;
 enum {
@@ -148,7 +149,10 @@ enum {
   ASMEVO_INJ_SET_NAN = 4,        /* canonical quiet NaN (float dtypes) */
   ASMEVO_INJ_SET_INF = 5,        /* +Inf (arg 0) or -Inf (arg 1); not for fp8 e4m3 */
   ASMEVO_INJ_GUARD_WRITE_LO = 6, /* invert `arg` canary bytes of the lo guard from byte `index` */
-  ASMEVO_INJ_GUARD_WRITE_HI = 7  /* same for the hi guard (an out-of-bounds write) */
+  ASMEVO_INJ_GUARD_WRITE_HI = 7, /* same for the hi guard (an out-of-bounds write) */
+  ASMEVO_INJ_PAD_WRITE = 8       /* invert `arg` row-pad bytes from data byte offset `index`
+                                    (a write past the end of a row); every byte named
+                                    must be padding of one row */
 };
 #define ASMEVO_INJ_RATE 0x100u
 enum { ASMEVO_SIDE_CANDIDATE = 0, ASMEVO_SIDE_BOTH = 1 };
@@ -286,17 +290,22 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
  * invalid). */
 size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n);
 
-/* Per-allocation guard result: counts of corrupted bytes and the lowest
- * corrupted byte offset within each guard (-1 if intact). */
+/* Per-allocation guard result (48 bytes): counts of corrupted bytes and the
+ * lowest corrupted byte offset within each guard (-1 if intact), and the same
+ * for the row padding, whose offsets count from the first data byte. */
 typedef struct {
   uint64_t bad_lo, bad_hi;
   int64_t first_bad_lo, first_bad_hi;
+  uint64_t bad_pad;
+  int64_t first_bad_pad;
 } asmevo_guard_result;
 
 /*
  * asmevo_guard_check -- compares every guard byte of the n allocations
  * against the canary regenerated from (seed, alloc_id) (the predicate iota
- * of section 3.2 requires intact out-of-bounds guards), writing results[0..n)
+ * of section 3.2 requires intact out-of-bounds guards), and every row-pad
+ * byte (elements cols..stride-1 of rows 0..rows-2, interior guards between
+ * rows) against the pad byte the fill wrote there, writing results[0..n)
  * (device memory).  Only the allocation geometry (base, rows, cols, stride,
  * guards, dtype, alloc_id) is used.  Errors: ASMEVO_E_INVALID,
  * ASMEVO_E_WORKSPACE.

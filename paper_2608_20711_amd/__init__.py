@@ -25,7 +25,7 @@ NAN_EQUAL, NAN_STRICT = 0, 1
 DIST_NORMAL, DIST_UNIFORM_INT, DIST_BITS, DIST_CONST, DIST_BOUNDARY = 0, 1, 2, 3, 4
 FILL_SATURATE = 1
 INJ_FLIP_BIT, INJ_STEP_WITHIN, INJ_SET_BEYOND, INJ_SET_NAN, INJ_SET_INF = 1, 2, 3, 4, 5
-INJ_GUARD_WRITE_LO, INJ_GUARD_WRITE_HI = 6, 7
+INJ_GUARD_WRITE_LO, INJ_GUARD_WRITE_HI, INJ_PAD_WRITE = 6, 7, 8
 INJ_RATE = 0x100
 SIDE_CANDIDATE, SIDE_BOTH = 0, 1
 
@@ -36,7 +36,7 @@ DIST_CODE = {"normal": DIST_NORMAL, "uniform_int": DIST_UNIFORM_INT, "bits": DIS
              "boundary": DIST_BOUNDARY}
 KIND_CODE = {"flip_bit": INJ_FLIP_BIT, "step_within": INJ_STEP_WITHIN, "set_beyond": INJ_SET_BEYOND,
              "set_nan": INJ_SET_NAN, "set_inf": INJ_SET_INF, "guard_write_lo": INJ_GUARD_WRITE_LO,
-             "guard_write_hi": INJ_GUARD_WRITE_HI}
+             "guard_write_hi": INJ_GUARD_WRITE_HI, "pad_write": INJ_PAD_WRITE}
 SIDE_CODE = {"candidate": SIDE_CANDIDATE, "both": SIDE_BOTH}
 
 
@@ -82,7 +82,8 @@ class Region(ctypes.Structure):
 
 class GuardResult(ctypes.Structure):
     _fields_ = [("bad_lo", ctypes.c_uint64), ("bad_hi", ctypes.c_uint64),
-                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64)]
+                ("first_bad_lo", ctypes.c_int64), ("first_bad_hi", ctypes.c_int64),
+                ("bad_pad", ctypes.c_uint64), ("first_bad_pad", ctypes.c_int64)]
 
 
 SEGMENT_RESULT_FIELDS = [f for f, _ in SegmentResult._fields_]

@@ -101,7 +101,7 @@ size_t asmevo_workspace_bytes(int32_t n_descs, int64_t n_inj) {
   const size_t n = n_descs > 0 ? (size_t)n_descs : 0;
   const size_t m = n_inj > 0 ? (size_t)n_inj : 0;
   return align256(n * sizeof(FillAlloc)) + align256(m * sizeof(FillRule)) +
-         align256(m * sizeof(PointEntry)) + align256(2 * n * sizeof(GuardRegion)) + 256;
+         align256(m * sizeof(PointEntry)) + align256(3 * n * sizeof(GuardRegion)) + 256;
 }
 
 // ---------------------------------------------------------------------------
@@ -186,10 +186,11 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
     const int es = esize_of(A.dtype);
     const bool rate = (J.kind & ASMEVO_INJ_RATE) != 0;
     const uint32_t kind = J.kind & ~ASMEVO_INJ_RATE;
-    if (kind < ASMEVO_INJ_FLIP_BIT || kind > ASMEVO_INJ_GUARD_WRITE_HI) return ASMEVO_E_INVALID;
+    if (kind < ASMEVO_INJ_FLIP_BIT || kind > ASMEVO_INJ_PAD_WRITE) return ASMEVO_E_INVALID;
     const bool guard = kind == ASMEVO_INJ_GUARD_WRITE_LO || kind == ASMEVO_INJ_GUARD_WRITE_HI;
-    if (guard && rate) return ASMEVO_E_INVALID;
-    if (!guard && kind != ASMEVO_INJ_FLIP_BIT && !is_float(A.dtype)) return ASMEVO_E_INVALID;
+    const bool pad = kind == ASMEVO_INJ_PAD_WRITE;
+    if ((guard || pad) && rate) return ASMEVO_E_INVALID;
+    if (!guard && !pad && kind != ASMEVO_INJ_FLIP_BIT && !is_float(A.dtype)) return ASMEVO_E_INVALID;
     if (kind == ASMEVO_INJ_SET_INF && A.dtype == ASMEVO_FP8_E4M3) return ASMEVO_E_UNSUPPORTED;
     if (kind == ASMEVO_INJ_FLIP_BIT && J.arg != 0xFFFFFFFFu && J.arg >= (uint32_t)(8 * es))
       return ASMEVO_E_INVALID;
@@ -209,6 +210,18 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
     if (guard) {
       const int64_t gsize = kind == ASMEVO_INJ_GUARD_WRITE_LO ? A.guard_lo : A.guard_hi;
       if (J.index < 0 || J.index + (int64_t)J.arg > gsize) return ASMEVO_E_INVALID;
+      if (applies && J.arg > 0)
+        points.push_back(PointEntry{J.alloc, kind, vsel, J.arg, J.index, J.atol, J.rtol});
+      continue;
+    }
+    if (pad) {
+      // the bytes must be padding of one row: [cols, stride) elements of a row below the last
+      const int64_t pitch = A.stride * es, row_data = A.cols * es;
+      if (J.index < 0 || pitch == 0) return ASMEVO_E_INVALID;
+      const int64_t r = J.index / pitch, off = J.index - r * pitch;
+      if (J.arg > 0 && (A.cols == 0 || r >= A.rows - 1 || off < row_data ||
+                        off + (int64_t)J.arg > pitch || J.index + (int64_t)J.arg > (int64_t)data_bytes(A)))
+        return ASMEVO_E_INVALID;
       if (applies && J.arg > 0)
         points.push_back(PointEntry{J.alloc, kind, vsel, J.arg, J.index, J.atol, J.rtol});
       continue;
@@ -473,6 +486,23 @@ asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t
       R.result_index = (uint32_t)k;
       regs.push_back(R);
       chunks += (g + kChunk - 1) / kChunk;
+    }
+    if (A.rows >= 2 && A.cols > 0 && A.stride > A.cols) {   // row padding: interior guards
+      if (A.base == 0) return ASMEVO_E_INVALID;
+      const uint64_t es = (uint64_t)esize_of(A.dtype);
+      GuardRegion R;
+      std::memset(&R, 0, sizeof(R));
+      R.addr = A.base + (uint64_t)A.guard_lo;
+      R.bytes = (uint64_t)(A.stride - A.cols) * es;
+      R.chunk_begin = chunks;
+      R.pitch = (uint64_t)A.stride * es;
+      R.pad_off = (uint64_t)A.cols * es;
+      R.run_chunks = (R.bytes + kChunk - 1) / kChunk;
+      R.alloc_id = A.alloc_id;
+      R.side = 2;
+      R.result_index = (uint32_t)k;
+      regs.push_back(R);
+      chunks += (uint64_t)(A.rows - 1) * R.run_chunks;
     }
   }
   const size_t bytes = std::max<size_t>(regs.size(), 1) * sizeof(GuardRegion);

@@ -443,8 +443,9 @@ __global__ __launch_bounds__(kFillBlock) void fill_kernel(const FillAlloc* __res
   }
 }
 
-// Point injections (deduplicated on the host: one entry per element) and
-// guard writes (bytes set to the complement of their canary).
+// Point injections (deduplicated on the host: one entry per element), guard
+// writes (bytes set to the complement of their canary) and row-pad writes
+// (bytes set to the complement of their pad byte).
 __global__ void inject_kernel(const FillAlloc* __restrict__ allocs,
                               const PointEntry* __restrict__ pts, int n_pts, uint64_t seed) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
@@ -457,6 +458,14 @@ __global__ void inject_kernel(const FillAlloc* __restrict__ allocs,
     for (uint32_t b = 0; b < P.arg; ++b) {
       const uint64_t p = (uint64_t)P.index + b;
       g[p] = (uint8_t)~canary_byte(A.alloc_id, side, p, seed);
+    }
+    return;
+  }
+  if (P.kind == ASMEVO_INJ_PAD_WRITE) {
+    AS_GLOBAL uint8_t* d = gptr_mut<uint8_t>(A.base + A.guard_lo);
+    for (uint32_t b = 0; b < P.arg; ++b) {
+      const uint64_t q = (uint64_t)P.index + b;
+      d[q] = (uint8_t)~pad_byte(A, q, seed);
     }
     return;
   }

@@ -1,8 +1,10 @@
 // guard.hip -- canary integrity check of guard regions (AsmEvo section 3.2:
 // the predicate iota requires intact out-of-bounds guards; section 3.4:
 // Tier-1 allocations carry canary-initialised guards, and guard regions are
-// checked byte-exactly).  The expected bytes are regenerated from
-// (seed, alloc_id, side), so only the candidate's guard bytes are read.
+// checked byte-exactly).  Row padding between the rows of a strided
+// allocation is checked the same way, as interior guards.  The expected
+// bytes are regenerated from (seed, alloc_id, side) -- the pad bytes from
+// the PAD stream at their data offset -- so only the candidate is read.
 #include "device_math.h"
 #include "kernels.h"
 #include "layout.h"
@@ -20,6 +22,8 @@ __global__ void guard_init_kernel(asmevo_guard_result* results, int n) {
   r.bad_hi = 0;
   r.first_bad_lo = -1;
   r.first_bad_hi = -1;
+  r.bad_pad = 0;
+  r.first_bad_pad = -1;
   results[t] = r;
 }
 
@@ -37,32 +41,60 @@ __global__ __launch_bounds__(256) void guard_kernel(const GuardRegion* __restric
       else hi = mid - 1;
     }
     const GuardRegion R = regs[lo];
-    const uint64_t p0 = (g - R.chunk_begin) * kChunk;
-    const uint64_t left = R.bytes - p0;
-    const uint32_t nb = left < (uint64_t)kChunk ? (uint32_t)left : (uint32_t)kChunk;
-    const U4 C = stream(seed, R.alloc_id, kCanary, R.side, 0, p0 >> 4);
-    const uint64_t src = R.addr + p0;
-    uint32_t mask = 0;
-    if (nb == (uint32_t)kChunk && (src & 15u) == 0) {
-      const u32x4 v = *gptr_mut<u32x4>(src);
-      const uint32_t x[4] = {v.x ^ C.x, v.y ^ C.y, v.z ^ C.z, v.w ^ C.w};
-#pragma unroll
-      for (int k = 0; k < 16; ++k) mask |= ((x[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? (1u << k) : 0u;
+    uint64_t p0, q0 = 0;            // byte offset in the guard (pad: in the run), pad data offset
+    uint32_t nb;
+    U4 C;
+    if (R.side < 2) {
+      p0 = (g - R.chunk_begin) * kChunk;
+      const uint64_t left = R.bytes - p0;
+      nb = left < (uint64_t)kChunk ? (uint32_t)left : (uint32_t)kChunk;
+      C = stream(seed, R.alloc_id, kCanary, R.side, 0, p0 >> 4);
     } else {
-      const AS_GLOBAL uint8_t* bytes = gptr_mut<uint8_t>(src);
-      for (uint32_t k = 0; k < nb; ++k)
-        mask |= (bytes[k] != byte_of(C, k)) ? (1u << k) : 0u;
+      const uint64_t k = g - R.chunk_begin;
+      const uint64_t run = k / R.run_chunks;
+      p0 = (k - run * R.run_chunks) * kChunk;
+      const uint64_t left = R.bytes - p0;
+      nb = left < (uint64_t)kChunk ? (uint32_t)left : (uint32_t)kChunk;
+      q0 = run * R.pitch + R.pad_off + p0;
+      C = stream(seed, R.alloc_id, kPad, 0, 0, q0 >> 4);
+    }
+    uint32_t mask = 0;
+    if (R.side < 2) {
+      const uint64_t src = R.addr + p0;
+      if (nb == (uint32_t)kChunk && (src & 15u) == 0) {
+        const u32x4 v = *gptr_mut<u32x4>(src);
+        const uint32_t x[4] = {v.x ^ C.x, v.y ^ C.y, v.z ^ C.z, v.w ^ C.w};
+#pragma unroll
+        for (int k = 0; k < 16; ++k) mask |= ((x[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? (1u << k) : 0u;
+      } else {
+        const AS_GLOBAL uint8_t* bytes = gptr_mut<uint8_t>(src);
+        for (uint32_t k = 0; k < nb; ++k)
+          mask |= (bytes[k] != byte_of(C, k)) ? (1u << k) : 0u;
+      }
+    } else {
+      // pad bytes [q0, q0 + nb) of the data region: PAD blocks q0 / 16 and the next
+      const AS_GLOBAL uint8_t* bytes = gptr_mut<uint8_t>(R.addr + q0);
+      const uint32_t ph = (uint32_t)(q0 & 15u);
+      const U4 C1 = stream(seed, R.alloc_id, kPad, 0, 0, (q0 >> 4) + 1u);
+      for (uint32_t k = 0; k < nb; ++k) {
+        const uint32_t j = ph + k;
+        const uint8_t want = j < 16u ? byte_of(C, j) : byte_of(C1, j - 16u);
+        mask |= (bytes[k] != want) ? (1u << k) : 0u;
+      }
     }
     if (mask) {
       asmevo_guard_result* res = results + R.result_index;
       const uint64_t cnt = (uint64_t)__builtin_popcount(mask);
-      const uint64_t first = p0 + (uint64_t)__builtin_ctz(mask);
+      const uint64_t first = (R.side < 2 ? p0 : q0) + (uint64_t)__builtin_ctz(mask);
       if (R.side == 0) {
         atomicAdd(reinterpret_cast<unsigned long long*>(&res->bad_lo), cnt);
         atomicMin(reinterpret_cast<unsigned long long*>(&res->first_bad_lo), first);
-      } else {
+      } else if (R.side == 1) {
         atomicAdd(reinterpret_cast<unsigned long long*>(&res->bad_hi), cnt);
         atomicMin(reinterpret_cast<unsigned long long*>(&res->first_bad_hi), first);
+      } else {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&res->bad_pad), cnt);
+        atomicMin(reinterpret_cast<unsigned long long*>(&res->first_bad_pad), first);
       }
     }
   }

@@ -92,14 +92,18 @@ struct CopyRegion {             // 64 bytes
 static_assert(sizeof(CopyRegion) == 64, "CopyRegion layout");
 
 // ---------------------------------------------------------------- guard
-struct GuardRegion {            // one guard side of one allocation
-  uint64_t addr;                // first guard byte
-  uint64_t bytes;
+// One guard side of one allocation, or (side 2) all row paddings of one
+// allocation: `runs` runs of `bytes` bytes, run r starting at data byte
+// r * pitch + pad_off; every run is cut into run_chunks 16-byte chunks.
+struct GuardRegion {            // 64 bytes
+  uint64_t addr;                // first guard byte; side 2: first data byte
+  uint64_t bytes;               // guard bytes; side 2: pad bytes per row
   uint64_t chunk_begin;         // first 16-byte chunk in the global chunk space
-  uint32_t alloc_id, side;      // side 0 = lo, 1 = hi
+  uint64_t pitch, pad_off;      // side 2: row pitch and pad start within a row, in bytes
+  uint64_t run_chunks;          // side 2: ceil(bytes / 16)
+  uint32_t alloc_id, side;      // side 0 = lo, 1 = hi, 2 = row padding
   uint32_t result_index, pad0;
-  uint32_t pad1, pad2;
 };
-static_assert(sizeof(GuardRegion) == 48, "GuardRegion layout");
+static_assert(sizeof(GuardRegion) == 64, "GuardRegion layout");
 
 }  // namespace asmevo

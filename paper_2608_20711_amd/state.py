@@ -22,7 +22,8 @@ SEG_RESULT_DTYPE = np.dtype([("mismatches", "<u8"), ("first_mismatch", "<i8"),
 COS_RESULT_DTYPE = np.dtype([("sum_ab", "<f8"), ("sum_aa", "<f8"), ("sum_bb", "<f8"), ("cosine", "<f8"),
                              ("pairs", "<u8"), ("blocks", "<u8")])
 GUARD_RESULT_DTYPE = np.dtype([("bad_lo", "<u8"), ("bad_hi", "<u8"),
-                               ("first_bad_lo", "<i8"), ("first_bad_hi", "<i8")])
+                               ("first_bad_lo", "<i8"), ("first_bad_hi", "<i8"),
+                               ("bad_pad", "<u8"), ("first_bad_pad", "<i8")])
 
 
 def injection_structs(w) -> List[Injection]:

@@ -61,7 +61,7 @@ def test_struct_layouts_match_header(tmp_path):
 
 def test_version_status_strings_workspace():
     L = lib.lib()
-    assert L.asmevo_abi_version() == 1
+    assert L.asmevo_abi_version() == 2
     for st in (lib.OK, lib.E_INVALID, lib.E_UNSUPPORTED, lib.E_WORKSPACE, lib.E_HIP):
         assert L.asmevo_status_string(st)
     assert lib.workspace_bytes(4096, 0) >= 4096 * 128
