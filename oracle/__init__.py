@@ -69,6 +69,18 @@ class RefSeg(ctypes.Structure):
                 ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
 
 
+MAX_DIMS = 8
+
+
+class RefSegND(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("nan_policy", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("index_base", ctypes.c_int64),
+                ("shape", ctypes.c_int64 * MAX_DIMS),
+                ("stride_a", ctypes.c_int64 * MAX_DIMS), ("stride_b", ctypes.c_int64 * MAX_DIMS),
+                ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
 class RefSegResult(ctypes.Structure):
     _fields_ = [("mismatches", ctypes.c_uint64), ("first_mismatch", ctypes.c_int64),
                 ("bitwise_mismatches", ctypes.c_uint64), ("first_bitwise", ctypes.c_int64),
@@ -129,6 +141,7 @@ def lib() -> ctypes.CDLL:
                                      ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
                                      ctypes.c_int64, vp]
         L.ref_diff_segment.argtypes = [P(RefSeg), vp, vp, P(RefSegResult)]
+        L.ref_diff_segment_nd.argtypes = [P(RefSegND), vp, vp, P(RefSegResult)]
         L.ref_cosine_segment.argtypes = [P(RefSeg), vp, vp, P(RefCosResult)]
         L.ref_pairwise_tree.argtypes = [vp, ctypes.c_int64]
         L.ref_pairwise_tree.restype = ctypes.c_double
@@ -291,6 +304,42 @@ def diff_segment(dtype: str, mode: str, nan_policy: str, rows: int, cols: int,
     if rc != 0:
         raise ValueError("oracle diff rejected the segment")
     return res.as_dict()
+
+
+def diff_segment_nd(dtype: str, mode: str, nan_policy: str, shape: Sequence[int],
+                    stride_a: Sequence[int], stride_b: Sequence[int], atol: float, rtol: float,
+                    a: np.ndarray, b: np.ndarray, a_off: int = 0, b_off: int = 0,
+                    index_base: int = 0) -> Dict:
+    """N-dimensional segment: shape and strides (in elements) of both
+    operands; a, b: uint8 arrays with element (0, ..., 0) at a_off / b_off."""
+    nd = len(shape)
+    assert nd <= MAX_DIMS and len(stride_a) == nd and len(stride_b) == nd
+    seg = RefSegND(DTYPE[dtype], MODE[mode], NAN_POLICY[nan_policy], nd, index_base,
+                   (ctypes.c_int64 * MAX_DIMS)(*shape), (ctypes.c_int64 * MAX_DIMS)(*stride_a),
+                   (ctypes.c_int64 * MAX_DIMS)(*stride_b), atol, rtol)
+    res = RefSegResult()
+    a = np.ascontiguousarray(a).view(np.uint8)
+    b = np.ascontiguousarray(b).view(np.uint8)
+    rc = lib().ref_diff_segment_nd(ctypes.byref(seg), _ptr(a) + a_off, _ptr(b) + b_off, ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle diff rejected the segment")
+    return res.as_dict()
+
+
+def merge_results(parts: Sequence[Dict]) -> Dict:
+    """One result for several segments that share it: counts add, first
+    indices take the lowest (ignoring -1), maxima take the largest."""
+    out = {"mismatches": 0, "first_mismatch": -1, "bitwise_mismatches": 0, "first_bitwise": -1,
+           "nonfinite_mismatches": 0, "max_abs": 0.0, "max_rel": 0.0}
+    for r in parts:
+        for f in ("mismatches", "bitwise_mismatches", "nonfinite_mismatches"):
+            out[f] += r[f]
+        for f in ("first_mismatch", "first_bitwise"):
+            if r[f] >= 0 and (out[f] < 0 or r[f] < out[f]):
+                out[f] = r[f]
+        for f in ("max_abs", "max_rel"):
+            out[f] = max(out[f], r[f])
+    return out
 
 
 def cosine_segment(dtype: str, rows: int, cols: int, stride_a: int, stride_b: int,

@@ -574,10 +574,7 @@ static uint64_t load_raw(const uint8_t* p, int es) {
   return v;
 }
 
-int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res) {
-  int es = ref_esize(seg->dtype);
-  if (es == 0) return -1;
-  if (seg->mode == REF_TOLERANCE && !is_float(seg->dtype)) return -1;
+static void result_reset(ref_seg_result* res) {
   res->mismatches = 0;
   res->first_mismatch = -1;
   res->bitwise_mismatches = 0;
@@ -585,50 +582,92 @@ int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref
   res->nonfinite_mismatches = 0;
   res->max_abs = 0.0;
   res->max_rel = 0.0;
+}
+
+/* One element pair at logical index i: the tolerance rule of the header, and
+ * the bitwise count.  Pairs are visited in increasing i, so the first index
+ * seen is the lowest. */
+static void compare_pair(int32_t dtype, int32_t mode, int32_t nan_policy, double atol, double rtol,
+                         uint64_t ra, uint64_t rb, int64_t i, ref_seg_result* res) {
+  int bitwise = ra != rb;
+  if (bitwise) {
+    res->bitwise_mismatches += 1;
+    if (res->first_bitwise < 0) res->first_bitwise = i;
+  }
+  int mismatch;
+  int nonfinite = 0;
+  if (mode == REF_BITWISE) {
+    mismatch = bitwise;
+  } else {
+    double A = 0.0, B = 0.0;
+    int ca = ref_decode(dtype, ra, &A);
+    int cb = ref_decode(dtype, rb, &B);
+    nonfinite = (ca != 0) || (cb != 0);
+    if (!bitwise) {
+      /* identical bits: a match, except a NaN under the strict policy */
+      mismatch = (cb == 3 && nan_policy == REF_NAN_STRICT);
+    } else if (ca == 3 || cb == 3) {
+      mismatch = !(ca == 3 && cb == 3 && nan_policy == REF_NAN_EQUAL);
+    } else if (nonfinite) {
+      mismatch = 1;   /* an infinity against anything with other bits */
+    } else {
+      double d = fabs(A - B);
+      double scaled = rtol * fabs(B);
+      double t = atol + scaled;
+      mismatch = !(d <= t);
+      double rel;
+      if (B != 0.0) rel = d / fabs(B);
+      else rel = (d == 0.0) ? 0.0 : INFINITY;
+      if (d > res->max_abs) res->max_abs = d;
+      if (rel > res->max_rel) res->max_rel = rel;
+    }
+  }
+  if (mismatch) {
+    res->mismatches += 1;
+    if (res->first_mismatch < 0) res->first_mismatch = i;
+    if (nonfinite) res->nonfinite_mismatches += 1;
+  }
+}
+
+int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res) {
+  int es = ref_esize(seg->dtype);
+  if (es == 0) return -1;
+  if (seg->mode == REF_TOLERANCE && !is_float(seg->dtype)) return -1;
+  result_reset(res);
   for (int64_t r = 0; r < seg->rows; ++r) {
     for (int64_t c = 0; c < seg->cols; ++c) {
       int64_t i = r * seg->cols + c;
       uint64_t ra = load_raw(a + (r * seg->stride_a + c) * es, es);
       uint64_t rb = load_raw(b + (r * seg->stride_b + c) * es, es);
-      int bitwise = ra != rb;
-      if (bitwise) {
-        res->bitwise_mismatches += 1;
-        if (res->first_bitwise < 0) res->first_bitwise = i;
-      }
-      int mismatch;
-      int nonfinite = 0;
-      if (seg->mode == REF_BITWISE) {
-        mismatch = bitwise;
-      } else {
-        double A = 0.0, B = 0.0;
-        int ca = ref_decode(seg->dtype, ra, &A);
-        int cb = ref_decode(seg->dtype, rb, &B);
-        nonfinite = (ca != 0) || (cb != 0);
-        if (!bitwise) {
-          /* identical bits: a match, except a NaN under the strict policy */
-          mismatch = (cb == 3 && seg->nan_policy == REF_NAN_STRICT);
-        } else if (ca == 3 || cb == 3) {
-          mismatch = !(ca == 3 && cb == 3 && seg->nan_policy == REF_NAN_EQUAL);
-        } else if (nonfinite) {
-          mismatch = 1;   /* an infinity against anything with other bits */
-        } else {
-          double d = fabs(A - B);
-          double scaled = seg->rtol * fabs(B);
-          double t = seg->atol + scaled;
-          mismatch = !(d <= t);
-          double rel;
-          if (B != 0.0) rel = d / fabs(B);
-          else rel = (d == 0.0) ? 0.0 : INFINITY;
-          if (d > res->max_abs) res->max_abs = d;
-          if (rel > res->max_rel) res->max_rel = rel;
-        }
-      }
-      if (mismatch) {
-        res->mismatches += 1;
-        if (res->first_mismatch < 0) res->first_mismatch = i;
-        if (nonfinite) res->nonfinite_mismatches += 1;
-      }
+      compare_pair(seg->dtype, seg->mode, seg->nan_policy, seg->atol, seg->rtol, ra, rb, i, res);
     }
+  }
+  return 0;
+}
+
+int ref_diff_segment_nd(const ref_seg_nd* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res) {
+  int es = ref_esize(seg->dtype);
+  if (es == 0 || seg->ndim < 0 || seg->ndim > REF_MAX_DIMS) return -1;
+  if (seg->mode == REF_TOLERANCE && !is_float(seg->dtype)) return -1;
+  result_reset(res);
+  int64_t total = 1;
+  for (int d = 0; d < seg->ndim; ++d) {
+    if (seg->shape[d] < 0 || seg->stride_a[d] < 0 || seg->stride_b[d] < 0) return -1;
+    total *= seg->shape[d];
+  }
+  for (int64_t i = 0; i < total; ++i) {
+    /* row-major multi-index of i: the last dimension varies fastest */
+    int64_t rest = i, off_a = 0, off_b = 0;
+    for (int d = seg->ndim - 1; d >= 0; --d) {
+      int64_t idx = rest % seg->shape[d];
+      rest /= seg->shape[d];
+      off_a += idx * seg->stride_a[d];
+      off_b += idx * seg->stride_b[d];
+    }
+    uint64_t ra = load_raw(a + off_a * es, es);
+    uint64_t rb = load_raw(b + off_b * es, es);
+    compare_pair(seg->dtype, seg->mode, seg->nan_policy, seg->atol, seg->rtol, ra, rb,
+                 seg->index_base + i, res);
   }
   return 0;
 }

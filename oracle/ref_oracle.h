@@ -60,6 +60,18 @@ typedef struct {
   double atol, rtol;
 } ref_seg;
 
+/* An N-dimensional segment: element (i_0, ..., i_{ndim-1}) of the candidate
+ * lies at a + sum_d i_d * stride_a[d] elements (b likewise); its logical
+ * index is index_base plus its row-major position (last dimension fastest). */
+#define REF_MAX_DIMS 8
+typedef struct {
+  int32_t dtype, mode, nan_policy, ndim;
+  int64_t index_base;
+  int64_t shape[REF_MAX_DIMS];
+  int64_t stride_a[REF_MAX_DIMS], stride_b[REF_MAX_DIMS];   /* elements, >= 0 */
+  double atol, rtol;
+} ref_seg_nd;
+
 typedef struct {
   uint64_t mismatches;
   int64_t first_mismatch;
@@ -101,6 +113,9 @@ int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64
 
 /* Compares one segment: a, b point at element (0,0) of candidate and reference. */
 int ref_diff_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res);
+
+/* Compares one N-dimensional segment: a, b point at element (0, ..., 0). */
+int ref_diff_segment_nd(const ref_seg_nd* seg, const uint8_t* a, const uint8_t* b, ref_seg_result* res);
 
 /* Guard check of one allocation: lo/hi point at the first byte of each guard (may be NULL if 0).
  * Sets bad_pad = 0 and first_bad_pad = -1. */
