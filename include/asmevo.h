@@ -16,6 +16,7 @@
  *   asmevo_diff_segments  element-wise compare of many buffers in one launch,
  *                         per-buffer counts / first index / max abs / max rel
  *                                                          (sec. 3.2, Eq. 1)
+ *                         (2-D segments; _nd: N-D shapes and strides)
  *   asmevo_guard_check    canary integrity of every guard region and of
  *                         the row padding                 (sec. 3.2 iota,
  *                                                          sec. 3.4)
@@ -245,6 +246,52 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
                                       asmevo_segment_result* results,
                                       void* workspace, size_t ws_bytes, void* stream,
                                       int32_t workgroups);
+
+/*
+ * One N-dimensional compared buffer pair (section 3.4: captured dispatch
+ * states hold non-contiguous tensors and block-table layouts; Tier-1 inputs
+ * span shapes and strides).  Element (i_0, ..., i_{ndim-1}) of the candidate
+ * lies at a + sum_d i_d * stride_a[d] elements (b likewise); its logical
+ * index is index_base plus its row-major position (the last dimension
+ * varies fastest).  0 <= ndim <= ASMEVO_MAX_DIMS (ndim 0: one element);
+ * shape[d] >= 0; strides >= 0 in elements (0 broadcasts; overlapping views
+ * are allowed, the operands are only read); a and b aligned to the element
+ * size; index_base >= 0.  `result` selects the entry of the results array
+ * this segment accumulates into: several segments may share one (a
+ * block-table layout: one segment per block, each with index_base = the
+ * block's logical start), and the shared entry then holds the summed
+ * counts, the lowest first indices and the largest maxima.  dtype, mode,
+ * nan_policy, atol and rtol as in asmevo_segment.
+ */
+#define ASMEVO_MAX_DIMS 8
+typedef struct {
+  uint64_t a, b;
+  uint32_t dtype, mode, nan_policy, ndim;
+  uint32_t result, reserved;
+  int64_t index_base;
+  int64_t shape[ASMEVO_MAX_DIMS];
+  int64_t stride_a[ASMEVO_MAX_DIMS];
+  int64_t stride_b[ASMEVO_MAX_DIMS];
+  double atol, rtol;
+} asmevo_segment_nd;
+
+/* Workspace bytes asmevo_diff_segments_nd needs for n segments. */
+size_t asmevo_diff_nd_workspace_bytes(int32_t n);
+
+/*
+ * asmevo_diff_segments_nd -- as asmevo_diff_segments for N-D segments, in one
+ * launch.  results[0..n_results) (device memory) are cleared first, then
+ * every segment accumulates into results[segs[k].result].  The planner drops
+ * unit dimensions and merges dimensions that are contiguous in both
+ * operands, so a contiguous tensor of any shape is one row and runs at the
+ * speed of the 1-D path.  The cosine term is not computed for N-D segments.
+ * Errors: ASMEVO_E_INVALID (also: result >= n_results, ndim out of range,
+ * negative shape, stride or index_base, an element offset beyond 2^52
+ * bytes), ASMEVO_E_WORKSPACE.
+ */
+asmevo_status asmevo_diff_segments_nd(const asmevo_segment_nd* segs, int32_t n,
+                                      asmevo_segment_result* results, int32_t n_results,
+                                      void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Cosine term of Eq. 1 (section 3.2): c_x = cos(K'(x), O(x)) per buffer,

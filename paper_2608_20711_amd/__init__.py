@@ -64,6 +64,31 @@ class Segment(ctypes.Structure):
                 ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
 
 
+MAX_DIMS = 8
+
+
+class SegmentND(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_uint64), ("b", ctypes.c_uint64),
+                ("dtype", ctypes.c_uint32), ("mode", ctypes.c_uint32),
+                ("nan_policy", ctypes.c_uint32), ("ndim", ctypes.c_uint32),
+                ("result", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("index_base", ctypes.c_int64),
+                ("shape", ctypes.c_int64 * MAX_DIMS),
+                ("stride_a", ctypes.c_int64 * MAX_DIMS), ("stride_b", ctypes.c_int64 * MAX_DIMS),
+                ("atol", ctypes.c_double), ("rtol", ctypes.c_double)]
+
+
+def segment_nd(a: int, b: int, dtype: int, mode: int, nan_policy: int, shape: Sequence[int],
+               stride_a: Sequence[int], stride_b: Sequence[int], atol: float = 0.0, rtol: float = 0.0,
+               result: int = 0, index_base: int = 0) -> SegmentND:
+    nd = len(shape)
+    if nd > MAX_DIMS or len(stride_a) != nd or len(stride_b) != nd:
+        raise ValueError("shape and strides must have the same length, at most 8")
+    arr = ctypes.c_int64 * MAX_DIMS
+    return SegmentND(a, b, dtype, mode, nan_policy, nd, result, 0, index_base, arr(*shape), arr(*stride_a),
+                     arr(*stride_b), atol, rtol)
+
+
 class SegmentResult(ctypes.Structure):
     _fields_ = [("mismatches", ctypes.c_uint64), ("first_mismatch", ctypes.c_int64),
                 ("bitwise_mismatches", ctypes.c_uint64), ("first_bitwise", ctypes.c_int64),
@@ -92,7 +117,8 @@ GUARD_RESULT_FIELDS = [f for f, _ in GuardResult._fields_]
 EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments_ex",
             "asmevo_diff_cosine", "asmevo_diff_cosine_workspace_bytes", "asmevo_copy_regions",
             "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
-            "asmevo_abi_version", "asmevo_last_hip_error"]
+            "asmevo_abi_version", "asmevo_last_hip_error", "asmevo_diff_segments_nd",
+            "asmevo_diff_nd_workspace_bytes"]
 
 
 class AsmevoError(RuntimeError):
@@ -124,6 +150,11 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_diff_segments_ex.restype = ctypes.c_int32
         L.asmevo_diff_cosine.argtypes = [P(Segment), ctypes.c_int32, vp, vp, vp, ctypes.c_size_t, vp]
         L.asmevo_diff_cosine.restype = ctypes.c_int32
+        L.asmevo_diff_segments_nd.argtypes = [P(SegmentND), ctypes.c_int32, vp, ctypes.c_int32, vp,
+                                              ctypes.c_size_t, vp]
+        L.asmevo_diff_segments_nd.restype = ctypes.c_int32
+        L.asmevo_diff_nd_workspace_bytes.argtypes = [ctypes.c_int32]
+        L.asmevo_diff_nd_workspace_bytes.restype = ctypes.c_size_t
         L.asmevo_diff_cosine_workspace_bytes.argtypes = [P(Segment), ctypes.c_int32]
         L.asmevo_diff_cosine_workspace_bytes.restype = ctypes.c_size_t
         L.asmevo_copy_regions.argtypes = [P(Region), ctypes.c_int32, vp, ctypes.c_size_t, vp]
@@ -186,6 +217,18 @@ def diff_segments(segments: Sequence[Segment], results_ptr: int, workspace_ptr: 
     _check(_lib().asmevo_diff_segments_ex(s, len(segments), results_ptr, workspace_ptr,
                                           workspace_size, _stream_handle(stream), workgroups),
            "asmevo_diff_segments")
+
+
+def diff_nd_workspace_bytes(n: int) -> int:
+    return int(_lib().asmevo_diff_nd_workspace_bytes(n))
+
+
+def diff_segments_nd(segments: Sequence[SegmentND], results_ptr: int, n_results: int, workspace_ptr: int,
+                     workspace_size: int, stream=None) -> None:
+    s = _array(SegmentND, segments)
+    _check(_lib().asmevo_diff_segments_nd(s, len(segments), results_ptr, n_results, workspace_ptr,
+                                          workspace_size, _stream_handle(stream)),
+           "asmevo_diff_segments_nd")
 
 
 def diff_cosine_workspace_bytes(segments: Sequence[Segment]) -> int:

@@ -338,6 +338,108 @@ asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled,
   return ASMEVO_OK;
 }
 
+// Validates N-D segments and builds their descriptors: unit dimensions are
+// dropped and dimensions contiguous in both operands merged, so the
+// innermost remaining dimension forms the rows and the others place them.
+asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_results,
+                           std::vector<DiffSeg>& dev, std::vector<NdExt>& ext, uint64_t& tiles) {
+  if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
+  dev.assign((size_t)n, DiffSeg{});
+  ext.assign((size_t)n, NdExt{});
+  tiles = 0;
+  struct Dim {
+    uint64_t n;
+    int64_t sa, sb;   // elements
+  };
+  for (int32_t k = 0; k < n; ++k) {
+    const asmevo_segment_nd& S = segs[k];
+    const int es = esize_of(S.dtype);
+    if (es == 0) return ASMEVO_E_INVALID;
+    if (S.mode != ASMEVO_BITWISE && S.mode != ASMEVO_TOLERANCE) return ASMEVO_E_INVALID;
+    if (S.nan_policy != ASMEVO_NAN_EQUAL && S.nan_policy != ASMEVO_NAN_STRICT) return ASMEVO_E_INVALID;
+    if (S.mode == ASMEVO_TOLERANCE) {
+      if (!is_float(S.dtype)) return ASMEVO_E_INVALID;
+      if (!std::isfinite(S.atol) || !std::isfinite(S.rtol) || S.atol < 0 || S.rtol < 0)
+        return ASMEVO_E_INVALID;
+    }
+    if (S.ndim > (uint32_t)ASMEVO_MAX_DIMS || S.result >= (uint32_t)n_results || S.index_base < 0)
+      return ASMEVO_E_INVALID;
+    bool empty = false;
+    double count = 1.0, span_a = 0.0, span_b = 0.0;   // range checks in fp64, exact below
+    for (uint32_t d = 0; d < S.ndim; ++d) {
+      if (S.shape[d] < 0 || S.stride_a[d] < 0 || S.stride_b[d] < 0) return ASMEVO_E_INVALID;
+      if (S.shape[d] == 0) empty = true;
+      count *= (double)S.shape[d];
+      if (S.shape[d] > 0) {
+        span_a += (double)(S.shape[d] - 1) * (double)S.stride_a[d];
+        span_b += (double)(S.shape[d] - 1) * (double)S.stride_b[d];
+      }
+    }
+    DiffSeg& D = dev[k];
+    NdExt& X = ext[k];
+    std::memset(&D, 0, sizeof(D));
+    std::memset(&X, 0, sizeof(X));
+    D.a = S.a;
+    D.b = S.b;
+    D.atol = S.atol;
+    D.rtol = S.rtol;
+    D.dtype = S.dtype;
+    D.mode = S.mode;
+    D.esize = (uint32_t)es;
+    D.result_index = S.result;
+    D.tile_begin = tiles;
+    X.index_base = (uint64_t)S.index_base;
+    if (empty) continue;
+    if (!S.a || !S.b || (S.a % (uint64_t)es) != 0 || (S.b % (uint64_t)es) != 0) return ASMEVO_E_INVALID;
+    if ((span_a + 1.0) * es > 0x1p52 || (span_b + 1.0) * es > 0x1p52) return ASMEVO_E_INVALID;
+    if ((double)S.index_base + count > 0x1p62) return ASMEVO_E_INVALID;
+    std::vector<Dim> dims;
+    for (uint32_t d = 0; d < S.ndim; ++d)
+      if (S.shape[d] > 1) dims.push_back(Dim{(uint64_t)S.shape[d], S.stride_a[d], S.stride_b[d]});
+    std::vector<Dim> m;   // merged, innermost first
+    for (int d = (int)dims.size() - 1; d >= 0; --d) {
+      if (!m.empty() && dims[d].sa == (int64_t)m.back().n * m.back().sa &&
+          dims[d].sb == (int64_t)m.back().n * m.back().sb)
+        m.back().n *= dims[d].n;
+      else
+        m.push_back(dims[d]);
+    }
+    std::reverse(m.begin(), m.end());   // outermost first
+    if (m.empty()) m.push_back(Dim{1, 1, 1});
+    const Dim inner = m.back();
+    const bool unit = inner.sa == 1 && inner.sb == 1;
+    X.in_sa = (uint64_t)inner.sa * es;
+    X.in_sb = (uint64_t)inner.sb * es;
+    X.nouter = (uint32_t)(m.size() - 1);
+    uint64_t rows = 1;
+    bool pitches16 = true;
+    for (size_t d = 0; d + 1 < m.size(); ++d) {
+      X.oshape[d] = m[d].n;
+      X.opa[d] = (uint64_t)m[d].sa * es;
+      X.opb[d] = (uint64_t)m[d].sb * es;
+      pitches16 = pitches16 && X.opa[d] % 16 == 0 && X.opb[d] % 16 == 0;
+      rows *= m[d].n;
+    }
+    D.rows = rows;
+    D.cols = inner.n;
+    D.row_bytes = D.cols * es;
+    D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
+    D.full_chunks = D.row_bytes / kChunk;
+    const bool aligned = unit && S.a % 16 == 0 && S.b % 16 == 0 && pitches16;
+    const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
+    D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) | (unit ? 0u : kSegGather) |
+              ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
+    if (narrow) {
+      D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
+    } else {
+      const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;
+      D.tile_count = D.rows * tpr;
+    }
+    tiles += D.tile_count;
+  }
+  return ASMEVO_OK;
+}
+
 // Cosine workspace: descriptors | one non-finite pair counter per segment |
 // three doubles per tile.
 struct CosLayout {
@@ -378,6 +480,38 @@ asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
                                    asmevo_segment_result* results, void* workspace,
                                    size_t ws_bytes, void* stream) {
   return asmevo_diff_segments_ex(segs, n, results, workspace, ws_bytes, stream, 0);
+}
+
+size_t asmevo_diff_nd_workspace_bytes(int32_t n) {
+  const size_t m = n > 0 ? (size_t)n : 0;
+  return align256(m * sizeof(DiffSeg)) + align256(m * sizeof(NdExt)) + 256;
+}
+
+asmevo_status asmevo_diff_segments_nd(const asmevo_segment_nd* segs, int32_t n,
+                                      asmevo_segment_result* results, int32_t n_results,
+                                      void* workspace, size_t ws_bytes, void* stream) {
+  if (n < 0 || n_results < 0 || (n > 0 && !segs) || (n_results > 0 && !results)) return ASMEVO_E_INVALID;
+  std::vector<DiffSeg> dev;
+  std::vector<NdExt> ext;
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff_nd(segs, n, n_results, dev, ext, tiles);
+  if (st != ASMEVO_OK) return st;
+  if (n_results == 0) return ASMEVO_OK;
+  const size_t off_ext = align256(dev.size() * sizeof(DiffSeg));
+  const size_t bytes = off_ext + ext.size() * sizeof(NdExt);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  if (n > 0) {
+    if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+    std::vector<uint8_t> host(bytes, 0);
+    put(host, 0, dev);
+    put(host, off_ext, ext);
+    HIP_TRY(hipMemcpyAsync(ws, host.data(), bytes, hipMemcpyHostToDevice, s));
+  }
+  const int wg = device_cus() * diff_nd_blocks_per_cu();
+  HIP_TRY(launch_diff_nd(reinterpret_cast<const DiffSeg*>(ws), reinterpret_cast<const NdExt*>(ws + off_ext),
+                         n, n_results, tiles, results, wg, s));
+  return ASMEVO_OK;
 }
 
 size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n) {

@@ -203,6 +203,72 @@ __device__ __forceinline__ void load_chunk(const uint8_t* pa, const uint8_t* pb,
   }
 }
 
+// Elements of a chunk `step` bytes apart (N-D segments whose innermost
+// dimension is not unit-stride); invalid elements read as zero on both sides.
+template <int DT>
+__device__ __forceinline__ u32x4 load_elems_strided(const uint8_t* p, uint32_t nv, uint64_t step) {
+  constexpr int es = Et<DT>::es;
+  constexpr int epc = 16 / es;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < epc; ++e) {
+    if ((uint32_t)e < nv) {
+      const uint8_t* q = p + (uint64_t)e * step;
+      if constexpr (es == 1) w[e >> 2] |= (uint32_t)*gptr<uint8_t>(q) << (8 * (e & 3));
+      else if constexpr (es == 2) w[e >> 1] |= (uint32_t)*gptr<uint16_t>(q) << (16 * (e & 1));
+      else if constexpr (es == 4) w[e] = *gptr<uint32_t>(q);
+      else {
+        const uint64_t raw = *gptr<uint64_t>(q);
+        w[2 * e] = (uint32_t)raw;
+        w[2 * e + 1] = (uint32_t)(raw >> 32);
+      }
+    }
+  }
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
+// Chunk c of a row of an N-D segment whose rows start at pa / pb.
+template <int DT>
+__device__ __forceinline__ void load_nd_chunk(const uint8_t* pa, const uint8_t* pb, uint64_t c,
+                                              uint32_t nbytes, bool vec, bool gather, uint64_t in_sa,
+                                              uint64_t in_sb, u32x4& va, u32x4& vb) {
+  if (gather) {
+    constexpr int epc = 16 / Et<DT>::es;
+    const uint32_t nv = nbytes / Et<DT>::es;
+    va = load_elems_strided<DT>(pa + c * epc * in_sa, nv, in_sa);
+    vb = load_elems_strided<DT>(pb + c * epc * in_sb, nv, in_sb);
+  } else {
+    load_chunk<DT>(pa + c * kChunk, pb + c * kChunk, nbytes, vec, va, vb);
+  }
+}
+
+// n / d and n % d, in 32 bits when both fit.
+__device__ __forceinline__ void divmod(uint64_t n, uint64_t d, uint64_t& q, uint64_t& r) {
+  if (((n | d) >> 32) == 0) {
+    const uint32_t q32 = (uint32_t)n / (uint32_t)d;
+    q = q32;
+    r = n - (uint64_t)q32 * d;
+  } else {
+    q = n / d;
+    r = n - q * d;
+  }
+}
+
+// Byte offsets of row r of an N-D segment in both operands.
+__device__ __forceinline__ void nd_row_offsets(const NdExt* X, uint64_t r, uint64_t& oa, uint64_t& ob) {
+  oa = 0;
+  ob = 0;
+  const int nd = (int)X->nouter;
+#pragma unroll 1
+  for (int d = nd - 1; d >= 0; --d) {
+    uint64_t q, idx;
+    divmod(r, X->oshape[d], q, idx);
+    oa += idx * X->opa[d];
+    ob += idx * X->opb[d];
+    r = q;
+  }
+}
+
 // ------------------------------------------------------------ cosine sums
 // Lane sums of one 4096-byte block (a*b, a*a, b*b over pairs with both
 // values finite).  Products of two values of any float element type are
@@ -330,10 +396,11 @@ __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
 }
 
 // All tiles [t_begin, t_end) of one segment.  COS: also the block sums of
-// each tile into `partials` (three doubles per global tile index).
-template <int DT, bool COS>
-__device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, uint64_t t_end,
-                                           uint32_t lane, Acc& acc, double* partials,
+// each tile into `partials` (three doubles per global tile index).  ND: rows
+// are placed by the segment's N-D extension X (the 2-D code otherwise).
+template <int DT, bool COS, bool ND>
+__device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
+                                           uint64_t t_end, uint32_t lane, Acc& acc, double* partials,
                                            uint32_t& nonfinite) {
   constexpr int es = Et<DT>::es;
   constexpr int epc = 16 / es;
@@ -344,6 +411,14 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
   const bool vec = (S.flags & kSegVec) != 0;
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
+  uint64_t ibase0 = 0, in_sa = 0, in_sb = 0;
+  bool gather = false;
+  if constexpr (ND) {
+    ibase0 = X->index_base;
+    in_sa = X->in_sa;
+    in_sb = X->in_sb;
+    gather = (S.flags & kSegGather) != 0;
+  }
 
   if (!kCos && (S.flags & kSegNarrow)) {
     // Short rows: tiles over the row-major chunk space, each lane finds its row.
@@ -357,13 +432,24 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
         uint32_t nb = 0;
         uint64_t i0 = 0;
         if (k < total) {
-          const uint64_t r = k / S.row_chunks;
-          const uint64_t c = k - r * S.row_chunks;
+          uint64_t r, c;
+          if constexpr (ND) {
+            divmod(k, S.row_chunks, r, c);
+          } else {
+            r = k / S.row_chunks;
+            c = k - r * S.row_chunks;
+          }
           const uint64_t cb = c * kChunk;
           const uint64_t rem = S.row_bytes - cb;
           nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-          load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb, vec, va, vb);
-          i0 = r * S.cols + c * epc;
+          if constexpr (ND) {
+            uint64_t oa, ob;
+            nd_row_offsets(X, r, oa, ob);
+            load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb, vec, gather, in_sa, in_sb, va, vb);
+          } else {
+            load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb, vec, va, vb);
+          }
+          i0 = ibase0 + r * S.cols + c * epc;
         }
         chunk<DT>(va, vb, i0, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
       }
@@ -372,16 +458,29 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
   }
 
   // Row-tiled: every tile lies inside one row (and is one cosine block).
-  const uint64_t tpr = S.tiles_per_row;
+  const uint64_t tpr = ND ? (S.row_chunks + kTileChunks - 1) / kTileChunks : (uint64_t)S.tiles_per_row;
   for (uint64_t tile = t_begin; tile < t_end; ++tile) {
     uint64_t r = 0, kt = tile;
     if (S.rows > 1) {
-      r = (uint32_t)tile / (uint32_t)tpr;
-      kt = tile - r * tpr;
+      if constexpr (ND) {
+        divmod(tile, tpr, r, kt);
+      } else {
+        r = (uint32_t)tile / (uint32_t)tpr;
+        kt = tile - r * tpr;
+      }
     }
-    const uint8_t* pa = a0 + r * S.a_pitch;
-    const uint8_t* pb = b0 + r * S.b_pitch;
-    const uint64_t ibase = r * S.cols;
+    const uint8_t* pa;
+    const uint8_t* pb;
+    if constexpr (ND) {
+      uint64_t oa, ob;
+      nd_row_offsets(X, r, oa, ob);
+      pa = a0 + oa;
+      pb = b0 + ob;
+    } else {
+      pa = a0 + r * S.a_pitch;
+      pb = b0 + r * S.b_pitch;
+    }
+    const uint64_t ibase = ibase0 + r * S.cols;
     const uint64_t k0 = kt * (uint64_t)kTileChunks;
     Cos cs{0.0, 0.0, 0.0};
     if (vec && k0 + kTileChunks <= S.full_chunks) {
@@ -425,7 +524,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, uint64_t t_begin, u
         const uint64_t cb = c * kChunk;
         const uint64_t rem = S.row_bytes - cb;
         nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-        load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
+        if constexpr (ND) load_nd_chunk<DT>(pa, pb, c, nb, vec, gather, in_sa, in_sb, va, vb);
+        else load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
       }
       chunk<DT>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
       if constexpr (kCos) cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
@@ -512,11 +612,11 @@ __global__ void diff_init_kernel(asmevo_segment_result* results, int n,
 }
 
 
-template <bool COS>
+template <bool COS, bool ND>
 __global__ __launch_bounds__(kDiffBlock)
 __attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU : ASMEVO_DIFF_WAVES_PER_EU)))
-void diff_kernel(const DiffSeg* __restrict__ segs, int n, uint64_t total_tiles,
-                 asmevo_segment_result* results, double* partials,
+void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
+                 uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                  unsigned long long* nonfinite_pairs) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = (uint64_t)blockIdx.x * (kDiffBlock / kWave) +
@@ -542,14 +642,17 @@ void diff_kernel(const DiffSeg* __restrict__ segs, int n, uint64_t total_tiles,
     const uint64_t seg_end = S.tile_begin + S.tile_count;
     const uint64_t t_end = seg_end < hi ? seg_end : hi;
     const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
+    const NdExt* X = ND ? ext + s : nullptr;
     switch (S.dtype) {
-      case ASMEVO_F32: diff_range<ASMEVO_F32, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_F16: diff_range<ASMEVO_F16, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_FP8_E4M3: diff_range<ASMEVO_FP8_E4M3, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_I32: diff_range<ASMEVO_I32, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_I64: diff_range<ASMEVO_I64, COS>(S, b, e, lane, acc, partials, nonfinite); break;
-      default: diff_range<ASMEVO_U8, COS>(S, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_FP8_E4M3:
+        diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite);
+        break;
+      case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
     }
     flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
     t = t_end;
@@ -663,7 +766,16 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 
 int diff_blocks_per_cu() {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false>, kDiffBlock, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false, false>, kDiffBlock, 0) !=
+          hipSuccess ||
+      blocks <= 0)
+    blocks = 4;
+  return blocks;
+}
+
+int diff_nd_blocks_per_cu() {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false, true>, kDiffBlock, 0) !=
           hipSuccess ||
       blocks <= 0)
     blocks = 4;
@@ -684,11 +796,11 @@ hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
     const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
     const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
     if (cos)
-      hipLaunchKernelGGL(diff_kernel<true>, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n, total_tiles,
-                         results, partials, nonfinite_pairs);
+      hipLaunchKernelGGL((diff_kernel<true, false>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, nullptr,
+                         n, total_tiles, results, partials, nonfinite_pairs);
     else
-      hipLaunchKernelGGL(diff_kernel<false>, dim3(wg), dim3(kDiffBlock), 0, stream, segs, n,
-                         total_tiles, results, nullptr, nullptr);
+      hipLaunchKernelGGL((diff_kernel<false, false>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, nullptr,
+                         n, total_tiles, results, nullptr, nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -698,6 +810,23 @@ hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
     e = hipGetLastError();
   }
   return e;
+}
+
+hipError_t launch_diff_nd(const DiffSeg* segs, const NdExt* ext, int n, int n_results,
+                          uint64_t total_tiles, asmevo_segment_result* results, int workgroups,
+                          hipStream_t stream) {
+  if (n_results > 0) {
+    hipLaunchKernelGGL(diff_init_kernel, dim3((n_results + 255) / 256), dim3(256), 0, stream, results,
+                       n_results, nullptr);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (n == 0 || total_tiles == 0) return hipSuccess;
+  const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
+  const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
+  hipLaunchKernelGGL((diff_kernel<false, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
+                     total_tiles, results, nullptr, nullptr);
+  return hipGetLastError();
 }
 
 }  // namespace asmevo

@@ -22,6 +22,13 @@ hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        double* partials = nullptr, unsigned long long* nonfinite_pairs = nullptr,
                        asmevo_cosine_result* cos_results = nullptr);
 
+// Resident N-D diff workgroups per compute unit.
+int diff_nd_blocks_per_cu();
+// Diff of N-D segments (descriptor k extended by ext[k]); zeroes results[0, n_results) first.
+hipError_t launch_diff_nd(const DiffSeg* segs, const NdExt* ext, int n, int n_results,
+                          uint64_t total_tiles, asmevo_segment_result* results, int workgroups,
+                          hipStream_t stream);
+
 hipError_t launch_copy(const CopyRegion* regs, int n, uint64_t total_tiles, int workgroups,
                        hipStream_t stream);
 

@@ -29,6 +29,7 @@ enum : uint32_t {
   kSegVec = 1u,       // a, b and both row pitches are 16-byte aligned
   kSegStrict = 4u,    // TOLERANCE with the strict NaN policy
   kSegNarrow = 8u,    // short 2-D rows: tiles run over the flattened chunk space
+  kSegGather = 16u,   // N-D: the innermost dimension is not unit-stride in a or b
 };
 
 // A segment is either "row-tiled" (every tile lies inside one row: contiguous
@@ -49,6 +50,22 @@ struct DiffSeg {                // 128 bytes
   uint32_t result_index, tiles_per_row;
 };
 static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
+
+// N-D segments: the DiffSeg describes rows of `cols` elements of the
+// innermost dimension (after dropping unit dimensions and merging dimensions
+// contiguous in both operands); this extension places row r: r is decomposed
+// over the outer dimensions (last one fastest) and each index is scaled by
+// that dimension's byte pitch.  Within a row, element j lies at j * in_sa
+// (in_sb) bytes.  Reported indices are index_base + r * cols + j.
+constexpr int kMaxOuter = 7;
+struct NdExt {                  // 200 bytes
+  uint64_t index_base;
+  uint64_t in_sa, in_sb;        // innermost-dimension strides in bytes
+  uint32_t nouter, pad0;
+  uint64_t oshape[kMaxOuter];   // outer dimensions, outermost first
+  uint64_t opa[kMaxOuter], opb[kMaxOuter];
+};
+static_assert(sizeof(NdExt) == 200, "NdExt layout");
 
 // ---------------------------------------------------------------- fill
 constexpr int kMaxRules = 16;      // Bernoulli rules per allocation

@@ -39,6 +39,7 @@ def test_struct_layouts_match_header(tmp_path):
         "asmevo_alloc": lib.Alloc, "asmevo_injection": lib.Injection, "asmevo_segment": lib.Segment,
         "asmevo_segment_result": lib.SegmentResult, "asmevo_guard_result": lib.GuardResult,
         "asmevo_cosine_result": lib.CosineResult, "asmevo_region": lib.Region,
+        "asmevo_segment_nd": lib.SegmentND,
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "asmevo.h"', "int main(void) {"]
     for cname, cls in fields.items():
@@ -57,6 +58,8 @@ def test_struct_layouts_match_header(tmp_path):
         for f, _ in cls._fields_:
             assert int(got[f"{cname}.{f}"]) == getattr(cls, f).offset, f"{cname}.{f}"
     assert ctypes.sizeof(lib.SegmentResult) == 56
+    assert ctypes.sizeof(lib.GuardResult) == 48
+    assert ctypes.sizeof(lib.SegmentND) == 256
 
 
 def test_version_status_strings_workspace():
@@ -137,6 +140,18 @@ def _inj(**kw):
     ([_alloc()], [_inj(kind=lib.INJ_SET_BEYOND, atol=-1.0)], lib.E_INVALID),
     ([_alloc()], [_inj(sides=2)], lib.E_INVALID),
     ([_alloc()], [_inj(kind=lib.INJ_FLIP_BIT | lib.INJ_RATE, index=10)] * 17, lib.E_UNSUPPORTED),
+    ([_alloc(dist=lib.DIST_BOUNDARY, p0=1.5)], [], lib.E_INVALID),        # rate above 1
+    ([_alloc(dist=lib.DIST_BOUNDARY, p0=float("nan"))], [], lib.E_INVALID),
+    ([_alloc(dist=lib.DIST_BOUNDARY, p0=0.1, p1=float("inf"))], [], lib.E_INVALID),
+    ([_alloc()], [_inj(kind=lib.INJ_PAD_WRITE, index=0, arg=1)], lib.E_INVALID),   # one row: no padding
+    ([_alloc(rows=3, cols=10, stride=12)], [_inj(kind=lib.INJ_PAD_WRITE, index=36, arg=1)],
+     lib.E_INVALID),                                                      # a data byte of row 0
+    ([_alloc(rows=3, cols=10, stride=12)], [_inj(kind=lib.INJ_PAD_WRITE, index=40, arg=9)],
+     lib.E_INVALID),                                                      # runs into row 1
+    ([_alloc(rows=3, cols=10, stride=12)], [_inj(kind=lib.INJ_PAD_WRITE, index=2 * 48 + 40, arg=1)],
+     lib.E_INVALID),                                                      # the last row has no padding
+    ([_alloc(rows=3, cols=10, stride=12)], [_inj(kind=lib.INJ_PAD_WRITE | lib.INJ_RATE, index=40, arg=1)],
+     lib.E_INVALID),
 ])
 def test_fill_argument_errors_before_any_device_work(allocs, inj, status):
     with pytest.raises(lib.AsmevoError) as e:
@@ -198,3 +213,44 @@ def test_copy_regions_workspace():
     with pytest.raises(lib.AsmevoError) as e:
         lib.copy_regions([lib.Region(0x1000, 0x9000, 64)], 0x50000, 8, stream=0)
     assert e.value.status == lib.E_WORKSPACE
+
+
+def _seg_nd(shape=(4, 8), sa=(8, 1), sb=(8, 1), **kw):
+    d = dict(a=0x10000, b=0x20000, dtype=lib.F32, mode=lib.TOLERANCE, nan_policy=0, shape=shape,
+             stride_a=sa, stride_b=sb)
+    d.update(kw)
+    return lib.segment_nd(**d)
+
+
+@pytest.mark.parametrize("seg,n_results", [
+    (_seg_nd(dtype=99), 1), (_seg_nd(mode=5), 1), (_seg_nd(nan_policy=2), 1),
+    (_seg_nd(result=1), 1),                                       # result slot out of range
+    (_seg_nd(shape=(4, -1), sa=(8, 1), sb=(8, 1)), 1),
+    (_seg_nd(sa=(8, -1)), 1),
+    (_seg_nd(index_base=-5), 1),
+    (_seg_nd(a=0x10002), 1),                                      # misaligned
+    (_seg_nd(b=0), 1),
+    (_seg_nd(shape=(1 << 40, 1 << 20), sa=(1 << 20, 1), sb=(1 << 20, 1)), 1),   # beyond 2^52 bytes
+    (_seg_nd(dtype=lib.U8, mode=lib.TOLERANCE), 1),
+    (_seg_nd(atol=-1.0), 1),
+])
+def test_diff_nd_argument_errors(seg, n_results):
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments_nd([seg], 0x40000, n_results, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+
+
+def test_diff_nd_ndim_and_workspace():
+    seg = _seg_nd()
+    seg.ndim = 9
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments_nd([seg], 0x40000, 1, 0x50000, 1 << 20, stream=0)
+    assert e.value.status == lib.E_INVALID
+    need = lib.diff_nd_workspace_bytes(3)
+    assert need >= 3 * (128 + 200)
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments_nd([_seg_nd()] * 3, 0x40000, 1, 0x50000, 3 * 128, stream=0)
+    assert e.value.status == lib.E_WORKSPACE
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.diff_segments_nd([_seg_nd()], 0, 1, 0x50000, need, stream=0)
+    assert e.value.status == lib.E_INVALID

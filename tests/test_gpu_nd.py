@@ -1,0 +1,162 @@
+"""GPU parity of N-dimensional segments (non-contiguous tensors and
+block-table layouts, paper section 3.4) against the oracle's N-D compare:
+transposed views (gathers), sliced views with long and short rows,
+broadcast dimensions, scalars, empty shapes, result slots shared by the
+blocks of a paged layout, every dtype, both NaN policies, and a larger
+sliced 3-D tensor.  Every byte a segment names is checked to lie inside its
+buffer before the launch."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_20711_amd as lib
+from gpu_helpers import assert_results_equal, log
+from paper_2608_20711_amd.state import SEG_RESULT_DTYPE
+
+pytestmark = pytest.mark.gpu
+
+NP_T = {"f32": np.float32, "f16": np.float16, "i32": np.int32, "i64": np.int64, "u8": np.uint8}
+
+
+def _extent_bytes(shape, strides, es):
+    if any(n == 0 for n in shape):
+        return 0
+    return (sum((n - 1) * s for n, s in zip(shape, strides)) + 1) * es
+
+
+def _run(specs, a_host: np.ndarray, b_host: np.ndarray, n_results=None):
+    """specs: dicts with dtype, mode, policy, shape, sa, sb, a_off, b_off, atol, rtol,
+    result, index_base.  Returns (gpu results, oracle results)."""
+    a_dev = torch.from_numpy(a_host.view(np.uint8).copy()).cuda()
+    b_dev = torch.from_numpy(b_host.view(np.uint8).copy()).cuda()
+    segs = []
+    n_results = n_results if n_results is not None else len(specs)
+    per_slot = [[] for _ in range(n_results)]
+    for s in specs:
+        es = oracle.ESIZE[oracle.DTYPE[s["dtype"]]]
+        assert s["a_off"] + _extent_bytes(s["shape"], s["sa"], es) <= a_dev.numel(), s
+        assert s["b_off"] + _extent_bytes(s["shape"], s["sb"], es) <= b_dev.numel(), s
+        segs.append(lib.segment_nd(a_dev.data_ptr() + s["a_off"], b_dev.data_ptr() + s["b_off"],
+                                   lib.DTYPE_CODE[s["dtype"]], lib.MODE_CODE[s["mode"]],
+                                   lib.NAN_CODE[s["policy"]], s["shape"], s["sa"], s["sb"], s["atol"],
+                                   s["rtol"], s["result"], s["index_base"]))
+        per_slot[s["result"]].append(
+            oracle.diff_segment_nd(s["dtype"], s["mode"], s["policy"], s["shape"], s["sa"], s["sb"], s["atol"],
+                                   s["rtol"], a_host.view(np.uint8), b_host.view(np.uint8), s["a_off"],
+                                   s["b_off"], s["index_base"]))
+    res = torch.empty(max(1, n_results) * SEG_RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    ws_size = lib.diff_nd_workspace_bytes(len(segs))
+    ws = torch.empty(ws_size, dtype=torch.uint8, device="cuda")
+    lib.diff_segments_nd(segs, res.data_ptr(), n_results, ws.data_ptr(), ws_size)
+    torch.cuda.synchronize()
+    raw = res.cpu().numpy()[: n_results * SEG_RESULT_DTYPE.itemsize].view(SEG_RESULT_DTYPE)
+    got = [{f: raw[f][k].item() for f in SEG_RESULT_DTYPE.names} for k in range(n_results)]
+    want = [oracle.merge_results(p) for p in per_slot]
+    return got, want
+
+
+def _spec(view, base_a, base_b, dtype, mode="tolerance", policy="equal", atol=1e-3, rtol=1e-3, result=0,
+          index_base=0, view_b=None):
+    view_b = view if view_b is None else view_b
+    es = view.itemsize
+    oa = view.__array_interface__["data"][0] - base_a.__array_interface__["data"][0]
+    ob = view_b.__array_interface__["data"][0] - base_b.__array_interface__["data"][0]
+    if dtype in ("i32", "i64", "u8"):
+        mode = "bitwise"
+    return dict(dtype=dtype, mode=mode, policy=policy, shape=list(view.shape),
+                sa=[s // es for s in view.strides], sb=[s // es for s in view_b.strides],
+                a_off=oa, b_off=ob, atol=atol, rtol=rtol, result=result, index_base=index_base)
+
+
+def _perturbed(base: np.ndarray, rng, frac=0.002, specials=True):
+    """A copy of `base` with a few elements changed (and NaN / Inf for floats)."""
+    out = base.copy()
+    flat = out.reshape(-1)
+    k = max(1, int(frac * flat.size))
+    idx = rng.choice(flat.size, size=k, replace=False)
+    if np.issubdtype(base.dtype, np.floating):
+        flat[idx] = (flat[idx].astype(np.float64) * (1 + rng.uniform(-0.01, 0.01, size=k))).astype(base.dtype)
+        if specials:
+            flat[idx[: k // 10]] = np.nan
+            flat[idx[k // 10: k // 5]] = np.inf
+    else:
+        flat[idx] ^= 1
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "i32", "i64", "u8"])
+def test_views_of_one_tensor(dtype):
+    rng = np.random.default_rng(11)
+    shape = (6, 10, 34, 50)
+    if dtype in ("f32", "f16"):
+        b = rng.standard_normal(shape).astype(NP_T[dtype])
+    else:
+        b = rng.integers(0, 100, size=shape).astype(NP_T[dtype])
+    a = _perturbed(b, rng)
+    views = [
+        lambda x: x,                                      # contiguous: one row
+        lambda x: x.transpose(0, 1, 3, 2),                # innermost not unit-stride: gather
+        lambda x: x.transpose(3, 2, 1, 0),
+        lambda x: x[1:5, ::3, 2:30, 7:45],                # sliced, short rows
+        lambda x: x[:, 2:9, :, :],                        # merges to long rows
+        lambda x: x[::2, :, 5, :],                        # a dropped dimension
+        lambda x: x[0, 0, 0, 0:1],                        # one element
+        lambda x: x[:, :, 3:3, :],                        # empty
+        lambda x: np.broadcast_to(x[:, :1, :, :], (6, 7, 34, 50)),   # broadcast
+    ]
+    specs = []
+    for k, v in enumerate(views):
+        for policy in ("equal", "strict"):
+            va, vb = v(a), v(b)
+            specs.append(_spec(va, a, b, dtype, policy=policy, result=len(specs), index_base=7 * k,
+                               view_b=vb))
+    got, want = _run(specs, a, b)
+    assert_results_equal(got, want, f"{dtype} views")
+    assert any(w["mismatches"] for w in want)
+
+
+def test_scalar_and_differently_strided_operands():
+    rng = np.random.default_rng(12)
+    b = rng.standard_normal((40, 60)).astype(np.float32)
+    a_full = _perturbed(np.ascontiguousarray(b.T), rng)          # candidate stored transposed
+    specs = [
+        _spec(a_full.T, a_full, b, "f32", view_b=b),               # a: column-major, b: row-major
+        dict(dtype="f32", mode="tolerance", policy="equal", shape=[], sa=[], sb=[], a_off=4 * 17, b_off=4 * 17,
+             atol=0.0, rtol=0.0, result=1, index_base=123),
+    ]
+    got, want = _run(specs, a_full, b)
+    assert_results_equal(got, want, "scalar / mixed strides")
+
+
+def test_block_table_segments_share_results():
+    """A paged cache of 48 physical blocks of 16 x 64 bf16-sized (f16) values;
+    two sequences, each a list of blocks; one segment per block, one result
+    per sequence."""
+    rng = np.random.default_rng(13)
+    n_phys, blk, width = 48, 16, 64
+    b = rng.standard_normal((n_phys, blk, width)).astype(np.float16)
+    a = _perturbed(b, rng, frac=0.001, specials=False)
+    order = rng.permutation(n_phys)
+    seqs = [order[:20].tolist(), order[20:45].tolist()]
+    specs = []
+    for s, table in enumerate(seqs):
+        for j, p in enumerate(table):
+            specs.append(_spec(a[p], a, b, "f16", result=s, index_base=j * blk * width, view_b=b[p]))
+    got, want = _run(specs, a, b, n_results=2)
+    assert_results_equal(got, want, "block table")
+    assert want[0]["mismatches"] > 0 and want[1]["mismatches"] > 0
+
+
+def test_larger_sliced_tensor():
+    rng = np.random.default_rng(14)
+    shape = (48, 96, 2048)
+    b = rng.standard_normal(shape).astype(np.float32)
+    a = _perturbed(b, rng, frac=1e-4)
+    log(f"nd large: {b.nbytes >> 20} MiB per side")
+    specs = [_spec(a[3:45, 10:90, 16:2000], a, b, "f32", result=0, view_b=b[3:45, 10:90, 16:2000]),
+             _spec(a[:, :, ::2], a, b, "f32", result=1, view_b=b[:, :, ::2]),
+             _spec(a.transpose(1, 0, 2)[:, :, :1024], a, b, "f32", result=2,
+                   view_b=b.transpose(1, 0, 2)[:, :, :1024])]
+    got, want = _run(specs, a, b)
+    assert_results_equal(got, want, "large sliced")
