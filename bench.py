@@ -64,6 +64,9 @@ def parse():
     p.add_argument("--cosine-steps", type=int, default=5,
                    help="after the timed steps, time the diff + cosine pass (Eq. 1's c_x) this many "
                         "times on the last candidate and report it beside the metric (0: skip)")
+    p.add_argument("--nd-steps", type=int, default=3,
+                   help="after the timed steps, time N-D views of the two states (sliced rows, a "
+                        "permuted 4-D layout, a transposed matrix, a stride-2 gather, a block table)")
     p.add_argument("--read-probe", type=int, default=-1, metavar="GIB",
                    help="after the timed steps, run the two-stream HBM read probe over GIB per "
                         "side and report it as the measured read ceiling (-1: the workload's "
@@ -120,6 +123,63 @@ def cpu_baseline(w, st, results, sample_bytes: float):
             "sample": f"{len(picked)} of {len(w.compares)} buffers, {acc / 2**30:.2f} GiB per side "
                       f"({compared / 2**30:.2f} GiB compared), diff only, {dt:.2f} s wall",
             "parity_with_gpu": bool(parity)}
+
+
+def nd_cases(st, stream, steps: int, scratch):
+    """Times asmevo_diff_segments_nd on views of the first (up to) 16 GiB of the
+    candidate and reference arenas, read as fp32 tensors."""
+    import numpy as np
+    import torch
+
+    import paper_2608_20711_amd as lib
+    from paper_2608_20711_amd.state import SEG_RESULT_DTYPE
+    n = min(st.cand.numel(), 16 << 30) // 4                     # fp32 elements per side
+    A, B = st.cand.data_ptr(), st.ref.data_ptr()
+    cases = {}
+    if n >= 64 * 4096:
+        r = n // (64 * 4096)
+        cases["sliced_rows"] = [([r, 64, 4032], [64 * 4096, 4096, 1], 0)]
+    h, s_, d = 32, 1024, 128
+    if n >= h * s_ * d:
+        cases["permuted_bhsd_as_bshd"] = [([n // (h * s_ * d), s_, h, d], [h * s_ * d, d, s_ * d, 1], 0)]
+    m = 16384
+    if n >= m * 16:
+        cases["transposed"] = [([n // m, m], [1, n // m], 0)]
+    cases["stride2_gather"] = [([n // 2], [2], 0)]
+    blk = 1 << 19                                              # 2 MiB blocks
+    if n >= 4 * blk:
+        order = np.random.default_rng(7).permutation(n // blk).tolist()
+        cases["block_table"] = [([1024, blk // 1024], [blk // 1024, 1], p * blk) for p in order]
+    res = torch.empty(SEG_RESULT_DTYPE.itemsize, dtype=torch.uint8, device=st.cand.device)
+    out = {}
+    for name, parts in cases.items():
+        segs = []
+        elems = 0
+        for j, (shape, strides, off) in enumerate(parts):
+            cnt = int(np.prod(shape))
+            span = (sum((k - 1) * v for k, v in zip(shape, strides)) + 1) * 4
+            assert off * 4 + span <= st.cand.numel() and off * 4 + span <= st.ref.numel(), name
+            segs.append(lib.segment_nd(A + off * 4, B + off * 4, lib.F32, lib.TOLERANCE, lib.NAN_EQUAL,
+                                       shape, strides, strides, 0.0, 0.0, 0, elems))
+            elems += cnt
+        ws = torch.empty(lib.diff_nd_workspace_bytes(len(segs)), dtype=torch.uint8, device=st.cand.device)
+        times = []
+        for _ in range(steps + 1):
+            if scratch is not None:
+                scratch.fill_(0x77)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            lib.diff_segments_nd(segs, res.data_ptr(), 1, ws.data_ptr(), ws.numel(), stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        med = statistics.median(times[1:])
+        gbps = 2 * 4 * elems / (med * 1e-3) / 1e9
+        out[name] = {"segments": len(segs), "shape": parts[0][0], "strides": parts[0][1],
+                     "logical_bytes_per_side": 4 * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
+                     "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2)}
+        del ws
+    return out
 
 
 def main():
@@ -256,6 +316,7 @@ def main():
                    "torch_copy_GBps_read_plus_write": round(2 * st.cand.numel() / (torch_copy_ms * 1e-3) / 1e9, 2)}
         del backup, rws
         torch.cuda.empty_cache()
+    nd = nd_cases(st, stream, args.nd_steps, scratch) if args.nd_steps > 0 else None
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 3),
@@ -275,6 +336,7 @@ def main():
                      "kernel": "diff_kernel (event span also holds the descriptor upload and result init)"},
         "diff_cosine": cosine,
         "restore": restore,
+        "diff_nd": nd,
         "total_mismatches": int(sum(r["mismatches"] for r in results)),
         "total_bitwise": int(sum(r["bitwise_mismatches"] for r in results)),
     }

@@ -338,9 +338,12 @@ asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled,
   return ASMEVO_OK;
 }
 
-// Validates N-D segments and builds their descriptors: unit dimensions are
-// dropped and dimensions contiguous in both operands merged, so the
-// innermost remaining dimension forms the rows and the others place them.
+// Validates N-D segments and builds their descriptors.  The dimensions are
+// ordered by decreasing stride of `a` (broadcast dimensions outermost), so the
+// walk follows memory; unit dimensions are dropped and dimensions contiguous
+// in both operands merged; the innermost remaining dimension forms the rows
+// and the others place them.  When the order differs from the logical one
+// the kernel maps walk positions back to logical indices on a mismatch.
 asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_results,
                            std::vector<DiffSeg>& dev, std::vector<NdExt>& ext, uint64_t& tiles) {
   if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
@@ -350,6 +353,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
   struct Dim {
     uint64_t n;
     int64_t sa, sb;   // elements
+    uint64_t lpitch;  // logical index pitch
   };
   for (int32_t k = 0; k < n; ++k) {
     const asmevo_segment_nd& S = segs[k];
@@ -394,18 +398,36 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     if ((span_a + 1.0) * es > 0x1p52 || (span_b + 1.0) * es > 0x1p52) return ASMEVO_E_INVALID;
     if ((double)S.index_base + count > 0x1p62) return ASMEVO_E_INVALID;
     std::vector<Dim> dims;
-    for (uint32_t d = 0; d < S.ndim; ++d)
-      if (S.shape[d] > 1) dims.push_back(Dim{(uint64_t)S.shape[d], S.stride_a[d], S.stride_b[d]});
+    uint64_t pitch = 1;
+    for (int d = (int)S.ndim - 1; d >= 0; --d) {
+      if (S.shape[d] > 1) dims.push_back(Dim{(uint64_t)S.shape[d], S.stride_a[d], S.stride_b[d], pitch});
+      pitch *= (uint64_t)S.shape[d];
+    }
+    std::reverse(dims.begin(), dims.end());   // logical order, outermost first
+    // walk order: decreasing stride of a, then of b; broadcast (stride 0) dimensions outermost
+    auto key = [](int64_t v) { return v == 0 ? INT64_MAX : v; };
+    std::vector<Dim> walk = dims;
+    std::stable_sort(walk.begin(), walk.end(), [&](const Dim& x, const Dim& y) {
+      if (key(x.sa) != key(y.sa)) return key(x.sa) > key(y.sa);
+      return key(x.sb) > key(y.sb);
+    });
+    bool permuted = false;
+    for (size_t d = 0; d < walk.size(); ++d) permuted = permuted || walk[d].lpitch != dims[d].lpitch;
+    X.ni = (uint32_t)walk.size();
+    for (size_t d = 0; d < walk.size(); ++d) {
+      X.ishape[d] = walk[d].n;
+      X.lpitch[d] = walk[d].lpitch;
+    }
     std::vector<Dim> m;   // merged, innermost first
-    for (int d = (int)dims.size() - 1; d >= 0; --d) {
-      if (!m.empty() && dims[d].sa == (int64_t)m.back().n * m.back().sa &&
-          dims[d].sb == (int64_t)m.back().n * m.back().sb)
-        m.back().n *= dims[d].n;
+    for (int d = (int)walk.size() - 1; d >= 0; --d) {
+      if (!m.empty() && walk[d].sa == (int64_t)m.back().n * m.back().sa &&
+          walk[d].sb == (int64_t)m.back().n * m.back().sb)
+        m.back().n *= walk[d].n;
       else
-        m.push_back(dims[d]);
+        m.push_back(walk[d]);
     }
     std::reverse(m.begin(), m.end());   // outermost first
-    if (m.empty()) m.push_back(Dim{1, 1, 1});
+    if (m.empty()) m.push_back(Dim{1, 1, 1, 1});
     const Dim inner = m.back();
     const bool unit = inner.sa == 1 && inner.sb == 1;
     X.in_sa = (uint64_t)inner.sa * es;
@@ -428,6 +450,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     const bool aligned = unit && S.a % 16 == 0 && S.b % 16 == 0 && pitches16;
     const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
     D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) | (unit ? 0u : kSegGather) |
+              (permuted ? kSegPermuted : 0u) |
               ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
     if (narrow) {
       D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;

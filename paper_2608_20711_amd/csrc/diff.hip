@@ -137,11 +137,16 @@ __device__ __forceinline__ void pair_slow(uint64_t ra, uint64_t rb, uint64_t i, 
   }
 }
 
-// One 16-byte chunk pair holding `nvalid` elements starting at logical index i0.
-template <int DT>
+// Logical index of walk position q of a reordered N-D segment.
+__device__ __forceinline__ uint64_t nd_logical(const NdExt* X, uint64_t q);
+
+// One 16-byte chunk pair holding `nvalid` elements starting at logical index
+// i0 (walk position i0 of a reordered N-D segment when `permuted`).
+template <int DT, bool ND = false>
 __device__ __forceinline__ void chunk(const u32x4& va, const u32x4& vb, uint64_t i0,
                                       uint32_t nvalid, bool tol_mode, bool strict, double atol,
-                                      double rtol, Acc& acc) {
+                                      double rtol, Acc& acc, const NdExt* X = nullptr,
+                                      bool permuted = false) {
   const u32x4 x = va ^ vb;
   if (((x.x | x.y | x.z | x.w) == 0u) && !strict) return;   // the common case
   constexpr int es = Et<DT>::es;
@@ -156,8 +161,11 @@ __device__ __forceinline__ void chunk(const u32x4& va, const u32x4& vb, uint64_t
   while (mask) {
     const uint32_t e = (uint32_t)__builtin_ctz(mask);
     mask &= mask - 1u;
-    pair_slow<DT>(elem_dyn<DT>(va, e), elem_dyn<DT>(vb, e), i0 + (uint64_t)e, tol_mode, strict,
-                  atol, rtol, acc);
+    uint64_t i = i0 + (uint64_t)e;
+    if constexpr (ND) {
+      if (permuted) i = nd_logical(X, i);
+    }
+    pair_slow<DT>(elem_dyn<DT>(va, e), elem_dyn<DT>(vb, e), i, tol_mode, strict, atol, rtol, acc);
   }
 }
 
@@ -267,6 +275,19 @@ __device__ __forceinline__ void nd_row_offsets(const NdExt* X, uint64_t r, uint6
     ob += idx * X->opb[d];
     r = q;
   }
+}
+
+__device__ __forceinline__ uint64_t nd_logical(const NdExt* X, uint64_t q) {
+  uint64_t l = 0;
+  const int ni = (int)X->ni;
+#pragma unroll 1
+  for (int d = ni - 1; d >= 0; --d) {
+    uint64_t rest, idx;
+    divmod(q, X->ishape[d], rest, idx);
+    l += idx * X->lpitch[d];
+    q = rest;
+  }
+  return X->index_base + l;
 }
 
 // ------------------------------------------------------------ cosine sums
@@ -412,9 +433,10 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
   uint64_t ibase0 = 0, in_sa = 0, in_sb = 0;
-  bool gather = false;
+  bool gather = false, permuted = false;
   if constexpr (ND) {
-    ibase0 = X->index_base;
+    permuted = (S.flags & kSegPermuted) != 0;
+    ibase0 = permuted ? 0 : X->index_base;    // reordered: indices are mapped on a mismatch
     in_sa = X->in_sa;
     in_sb = X->in_sb;
     gather = (S.flags & kSegGather) != 0;
@@ -451,7 +473,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           }
           i0 = ibase0 + r * S.cols + c * epc;
         }
-        chunk<DT>(va, vb, i0, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
+        chunk<DT, ND>(va, vb, i0, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
       }
     }
     return;
@@ -499,8 +521,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       if (((x.x | x.y | x.z | x.w) != 0u) || strict) {
 #pragma unroll
         for (int j = 0; j < U; ++j)
-          chunk<DT>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
-                    strict, S.atol, S.rtol, acc);
+          chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
+                        strict, S.atol, S.rtol, acc, X, permuted);
       }
       if constexpr (kCos) {
 #pragma unroll
@@ -527,7 +549,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         if constexpr (ND) load_nd_chunk<DT>(pa, pb, c, nb, vec, gather, in_sa, in_sb, va, vb);
         else load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
       }
-      chunk<DT>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc);
+      chunk<DT, ND>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
       if constexpr (kCos) cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
     }
     if constexpr (kCos) cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);

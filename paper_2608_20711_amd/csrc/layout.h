@@ -30,6 +30,7 @@ enum : uint32_t {
   kSegStrict = 4u,    // TOLERANCE with the strict NaN policy
   kSegNarrow = 8u,    // short 2-D rows: tiles run over the flattened chunk space
   kSegGather = 16u,   // N-D: the innermost dimension is not unit-stride in a or b
+  kSegPermuted = 32u, // N-D: visited in memory order, not logical order (see NdExt)
 };
 
 // A segment is either "row-tiled" (every tile lies inside one row: contiguous
@@ -51,21 +52,30 @@ struct DiffSeg {                // 128 bytes
 };
 static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
 
-// N-D segments: the DiffSeg describes rows of `cols` elements of the
-// innermost dimension (after dropping unit dimensions and merging dimensions
-// contiguous in both operands); this extension places row r: r is decomposed
-// over the outer dimensions (last one fastest) and each index is scaled by
-// that dimension's byte pitch.  Within a row, element j lies at j * in_sa
-// (in_sb) bytes.  Reported indices are index_base + r * cols + j.
+// N-D segments.  The planner orders the dimensions by decreasing stride of
+// `a` (broadcast dimensions outermost) so that the walk follows memory, then
+// drops unit dimensions and merges dimensions contiguous in both operands.
+// The DiffSeg describes rows of `cols` elements of the innermost remaining
+// dimension; this extension places row r: r is decomposed over the outer
+// dimensions (last one fastest) and each index is scaled by that
+// dimension's byte pitch.  Within a row, element j lies at j * in_sa (in_sb)
+// bytes.  The walk position q = r * cols + j is the element's logical
+// (row-major) index when the order was not changed; otherwise (kSegPermuted)
+// q is decomposed over the ordered, unmerged dimensions ishape (last one
+// fastest) and the logical index is sum idx_d * lpitch[d].  Either way
+// index_base is added.
 constexpr int kMaxOuter = 7;
-struct NdExt {                  // 200 bytes
+constexpr int kMaxDims = 8;
+struct NdExt {                  // 328 bytes
   uint64_t index_base;
   uint64_t in_sa, in_sb;        // innermost-dimension strides in bytes
-  uint32_t nouter, pad0;
+  uint32_t nouter, ni;          // outer (merged) dimensions; ordered unmerged dimensions
   uint64_t oshape[kMaxOuter];   // outer dimensions, outermost first
   uint64_t opa[kMaxOuter], opb[kMaxOuter];
+  uint64_t ishape[kMaxDims];    // kSegPermuted: walk order, outermost first
+  uint64_t lpitch[kMaxDims];    // logical index pitch of each of them
 };
-static_assert(sizeof(NdExt) == 200, "NdExt layout");
+static_assert(sizeof(NdExt) == 328, "NdExt layout");
 
 // ---------------------------------------------------------------- fill
 constexpr int kMaxRules = 16;      // Bernoulli rules per allocation
