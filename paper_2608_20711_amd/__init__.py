@@ -177,10 +177,22 @@ def lib() -> ctypes.CDLL:
 
 
 def _array(cls, items: Sequence):
+    """A ctypes array of `cls` holding `items`; an array of `cls` built once by
+    the caller (see descriptor_array) is passed through unchanged."""
+    if isinstance(items, ctypes.Array) and items._type_ is cls:
+        return items
     arr = (cls * max(1, len(items)))()
     for k, it in enumerate(items):
         arr[k] = it
     return arr
+
+
+def descriptor_array(items: Sequence):
+    """Packs descriptors (all of one struct type) into a ctypes array once, for
+    callers that issue the same call many times."""
+    if not items:
+        raise ValueError("no descriptors")
+    return _array(type(items[0]), items)
 
 
 def _check(status: int, call: str):

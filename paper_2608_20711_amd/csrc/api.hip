@@ -348,13 +348,14 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
                            std::vector<DiffSeg>& dev, std::vector<NdExt>& ext, uint64_t& tiles) {
   if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
   dev.assign((size_t)n, DiffSeg{});
-  ext.assign((size_t)n, NdExt{});
+  ext.clear();
   tiles = 0;
   struct Dim {
     uint64_t n;
     int64_t sa, sb;   // elements
     uint64_t lpitch;  // logical index pitch
   };
+  uint64_t n_ext = 0;
   for (int32_t k = 0; k < n; ++k) {
     const asmevo_segment_nd& S = segs[k];
     const int es = esize_of(S.dtype);
@@ -380,7 +381,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
       }
     }
     DiffSeg& D = dev[k];
-    NdExt& X = ext[k];
+    NdExt X;
     std::memset(&D, 0, sizeof(D));
     std::memset(&X, 0, sizeof(X));
     D.a = S.a;
@@ -392,50 +393,65 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     D.esize = (uint32_t)es;
     D.result_index = S.result;
     D.tile_begin = tiles;
+    D.nd_index_base = (uint64_t)S.index_base;
+    D.nd_ext = ~0ull;
     X.index_base = (uint64_t)S.index_base;
     if (empty) continue;
     if (!S.a || !S.b || (S.a % (uint64_t)es) != 0 || (S.b % (uint64_t)es) != 0) return ASMEVO_E_INVALID;
     if ((span_a + 1.0) * es > 0x1p52 || (span_b + 1.0) * es > 0x1p52) return ASMEVO_E_INVALID;
     if ((double)S.index_base + count > 0x1p62) return ASMEVO_E_INVALID;
-    std::vector<Dim> dims;
+    // fixed-size arrays: planning many small segments (block tables) stays cheap
+    Dim dims[ASMEVO_MAX_DIMS], walk[ASMEVO_MAX_DIMS], m[ASMEVO_MAX_DIMS];
+    int nd = 0;
     uint64_t pitch = 1;
+    uint64_t pitches[ASMEVO_MAX_DIMS];
     for (int d = (int)S.ndim - 1; d >= 0; --d) {
-      if (S.shape[d] > 1) dims.push_back(Dim{(uint64_t)S.shape[d], S.stride_a[d], S.stride_b[d], pitch});
+      pitches[d] = pitch;
       pitch *= (uint64_t)S.shape[d];
     }
-    std::reverse(dims.begin(), dims.end());   // logical order, outermost first
-    // walk order: decreasing stride of a, then of b; broadcast (stride 0) dimensions outermost
+    for (uint32_t d = 0; d < S.ndim; ++d)   // logical order, outermost first
+      if (S.shape[d] > 1) dims[nd++] = Dim{(uint64_t)S.shape[d], S.stride_a[d], S.stride_b[d], pitches[d]};
+    // walk order: decreasing stride of a, then of b; broadcast (stride 0) dimensions outermost;
+    // a stable insertion sort
     auto key = [](int64_t v) { return v == 0 ? INT64_MAX : v; };
-    std::vector<Dim> walk = dims;
-    std::stable_sort(walk.begin(), walk.end(), [&](const Dim& x, const Dim& y) {
+    auto before = [&](const Dim& x, const Dim& y) {
       if (key(x.sa) != key(y.sa)) return key(x.sa) > key(y.sa);
       return key(x.sb) > key(y.sb);
-    });
+    };
+    for (int d = 0; d < nd; ++d) {
+      const Dim v = dims[d];
+      int j = d;
+      while (j > 0 && before(v, walk[j - 1])) {
+        walk[j] = walk[j - 1];
+        --j;
+      }
+      walk[j] = v;
+    }
     bool permuted = false;
-    for (size_t d = 0; d < walk.size(); ++d) permuted = permuted || walk[d].lpitch != dims[d].lpitch;
-    X.ni = (uint32_t)walk.size();
-    for (size_t d = 0; d < walk.size(); ++d) {
+    for (int d = 0; d < nd; ++d) permuted = permuted || walk[d].lpitch != dims[d].lpitch;
+    X.ni = (uint32_t)nd;
+    for (int d = 0; d < nd; ++d) {
       X.ishape[d] = walk[d].n;
       X.lpitch[d] = walk[d].lpitch;
     }
-    std::vector<Dim> m;   // merged, innermost first
-    for (int d = (int)walk.size() - 1; d >= 0; --d) {
-      if (!m.empty() && walk[d].sa == (int64_t)m.back().n * m.back().sa &&
-          walk[d].sb == (int64_t)m.back().n * m.back().sb)
-        m.back().n *= walk[d].n;
+    int nm = 0;   // merged, innermost first
+    for (int d = nd - 1; d >= 0; --d) {
+      if (nm > 0 && walk[d].sa == (int64_t)m[nm - 1].n * m[nm - 1].sa &&
+          walk[d].sb == (int64_t)m[nm - 1].n * m[nm - 1].sb)
+        m[nm - 1].n *= walk[d].n;
       else
-        m.push_back(walk[d]);
+        m[nm++] = walk[d];
     }
-    std::reverse(m.begin(), m.end());   // outermost first
-    if (m.empty()) m.push_back(Dim{1, 1, 1, 1});
-    const Dim inner = m.back();
+    std::reverse(m, m + nm);   // outermost first
+    if (nm == 0) m[nm++] = Dim{1, 1, 1, 1};
+    const Dim inner = m[nm - 1];
     const bool unit = inner.sa == 1 && inner.sb == 1;
     X.in_sa = (uint64_t)inner.sa * es;
     X.in_sb = (uint64_t)inner.sb * es;
-    X.nouter = (uint32_t)(m.size() - 1);
+    X.nouter = (uint32_t)(nm - 1);
     uint64_t rows = 1;
     bool pitches16 = true;
-    for (size_t d = 0; d + 1 < m.size(); ++d) {
+    for (int d = 0; d + 1 < nm; ++d) {
       X.oshape[d] = m[d].n;
       X.opa[d] = (uint64_t)m[d].sa * es;
       X.opb[d] = (uint64_t)m[d].sb * es;
@@ -452,6 +468,10 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) | (unit ? 0u : kSegGather) |
               (permuted ? kSegPermuted : 0u) |
               ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
+    if (D.rows > 1 || !unit || permuted) {   // only these segments read an extension
+      D.nd_ext = n_ext++;
+      ext.push_back(X);
+    }
     if (narrow) {
       D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
     } else {
@@ -459,6 +479,12 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
       D.tile_count = D.rows * tpr;
     }
     tiles += D.tile_count;
+  }
+  // the kernel reads an extension exactly for these segments: it must exist
+  for (int32_t k = 0; k < n; ++k) {
+    const DiffSeg& D = dev[k];
+    const bool needs = D.tile_count > 0 && (D.rows > 1 || (D.flags & (kSegGather | kSegPermuted)) != 0);
+    if (needs && D.nd_ext >= ext.size()) return ASMEVO_E_INVALID;
   }
   return ASMEVO_OK;
 }

@@ -436,10 +436,12 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
   bool gather = false, permuted = false;
   if constexpr (ND) {
     permuted = (S.flags & kSegPermuted) != 0;
-    ibase0 = permuted ? 0 : X->index_base;    // reordered: indices are mapped on a mismatch
-    in_sa = X->in_sa;
-    in_sb = X->in_sb;
+    ibase0 = permuted ? 0 : S.nd_index_base;  // reordered: indices are mapped on a mismatch
     gather = (S.flags & kSegGather) != 0;
+    if (X != nullptr) {
+      in_sa = X->in_sa;
+      in_sb = X->in_sb;
+    }
   }
 
   if (!kCos && (S.flags & kSegNarrow)) {
@@ -465,8 +467,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           const uint64_t rem = S.row_bytes - cb;
           nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
           if constexpr (ND) {
-            uint64_t oa, ob;
-            nd_row_offsets(X, r, oa, ob);
+            uint64_t oa = 0, ob = 0;
+            if (S.rows > 1) nd_row_offsets(X, r, oa, ob);   // a segment of several rows has an extension
             load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb, vec, gather, in_sa, in_sb, va, vb);
           } else {
             load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb, vec, va, vb);
@@ -494,8 +496,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     const uint8_t* pa;
     const uint8_t* pb;
     if constexpr (ND) {
-      uint64_t oa, ob;
-      nd_row_offsets(X, r, oa, ob);
+      uint64_t oa = 0, ob = 0;
+      if (S.rows > 1) nd_row_offsets(X, r, oa, ob);     // one row: no extension, offset 0
       pa = a0 + oa;
       pb = b0 + ob;
     } else {
@@ -664,7 +666,7 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
     const uint64_t seg_end = S.tile_begin + S.tile_count;
     const uint64_t t_end = seg_end < hi ? seg_end : hi;
     const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
-    const NdExt* X = ND ? ext + s : nullptr;
+    const NdExt* X = (ND && S.nd_ext != ~0ull) ? ext + S.nd_ext : nullptr;
     switch (S.dtype) {
       case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
       case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;

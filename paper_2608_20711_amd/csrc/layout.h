@@ -38,7 +38,14 @@ enum : uint32_t {
 // run over the row-major chunk space and each lane finds its own row).
 struct DiffSeg {                // 128 bytes
   uint64_t a, b;                // element (0,0) of candidate / reference
-  uint64_t a_pitch, b_pitch;    // bytes between row starts
+  union {
+    uint64_t a_pitch;           // 2-D: bytes between row starts
+    uint64_t nd_index_base;     // N-D: added to every reported index
+  };
+  union {
+    uint64_t b_pitch;
+    uint64_t nd_ext;            // N-D: index of the segment's NdExt; ~0 if it needs none
+  };
   uint64_t rows;                // 1 when the segment is contiguous in both operands
   uint64_t cols;                // logical elements per (possibly flattened) row
   uint64_t row_bytes;           // cols * esize
@@ -63,7 +70,8 @@ static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
 // (row-major) index when the order was not changed; otherwise (kSegPermuted)
 // q is decomposed over the ordered, unmerged dimensions ishape (last one
 // fastest) and the logical index is sum idx_d * lpitch[d].  Either way
-// index_base is added.
+// index_base is added.  A segment that is one row in memory order (rows == 1,
+// unit stride, no reordering) needs no extension.
 constexpr int kMaxOuter = 7;
 constexpr int kMaxDims = 8;
 struct NdExt {                  // 328 bytes
