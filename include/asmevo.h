@@ -392,6 +392,45 @@ int32_t asmevo_abi_version(void);
 /* hipError_t code of the last failing HIP call on this thread (0 if none). */
 int32_t asmevo_last_hip_error(void);
 
+/*
+ * Code objects under test (section 3.7, Algorithm 1: a candidate is built
+ * into a code object and, once its static checks pass, run under the same
+ * device and launch conditions as the original K0 for the equivalence check
+ * and the timing).  The caller builds the code objects; these calls load one,
+ * launch it with explicit arguments, and time it.
+ */
+typedef struct {
+  uint64_t module, function;     /* hipModule_t / hipFunction_t */
+  int32_t num_regs;              /* from the runtime's function attributes */
+  int32_t shared_bytes;          /* static LDS */
+  int32_t max_threads;           /* largest workgroup the code object accepts */
+  int32_t local_bytes;           /* scratch per work-item */
+} asmevo_kernel;
+
+/* Loads a code object image (an AMDGPU ELF, host memory, size image_bytes)
+ * and finds kernel `name`.  The caller owns the returned handle and frees it
+ * with asmevo_kernel_unload.  Errors: ASMEVO_E_INVALID for null arguments,
+ * ASMEVO_E_HIP when the runtime rejects the image or does not find the
+ * kernel (asmevo_last_hip_error gives the code). */
+asmevo_status asmevo_kernel_load(const void* image, size_t image_bytes, const char* name,
+                                 asmevo_kernel* out);
+asmevo_status asmevo_kernel_unload(asmevo_kernel* k);
+
+/* Enqueues one launch: grid in workgroups, block in work-items, dynamic LDS
+ * bytes, params[i] pointing at the value of explicit argument i (laid out by
+ * the runtime from the code object's metadata).  Errors: ASMEVO_E_INVALID
+ * for zero dimensions or a block larger than the kernel allows, ASMEVO_E_HIP. */
+asmevo_status asmevo_kernel_launch(const asmevo_kernel* k, const uint32_t grid[3],
+                                   const uint32_t block[3], uint32_t lds_bytes, void** params,
+                                   void* stream);
+
+/* `warmup` untimed launches, then `reps` launches each bracketed by HIP
+ * events on `stream`; waits for the stream and writes the reps durations in
+ * milliseconds to ms_out[0..reps). */
+asmevo_status asmevo_kernel_time(const asmevo_kernel* k, const uint32_t grid[3],
+                                 const uint32_t block[3], uint32_t lds_bytes, void** params,
+                                 int32_t warmup, int32_t reps, float* ms_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -418,6 +418,17 @@ def pad_check(w, k: int, data: np.ndarray) -> Dict:
     return {"bad_pad": res.bad_pad, "first_bad_pad": res.first_bad_pad}
 
 
+def pad_check_alloc(seed: int, alloc_id: int, dtype: str, rows: int, cols: int, stride: int,
+                    data: np.ndarray) -> Dict:
+    """Row-pad check of one allocation given by its geometry; `data` is its data region."""
+    data = np.ascontiguousarray(data, dtype=np.uint8)
+    a = RefAlloc(DTYPE[dtype], alloc_id, rows, cols, stride, 0, 0, 0, 0, 0.0, 0.0, 0, 0)
+    res = RefGuardResult()
+    if lib().ref_pad_check(ctypes.byref(a), seed, _ptr(data) if data.size else None, ctypes.byref(res)) != 0:
+        raise ValueError("oracle pad check rejected the allocation")
+    return {"bad_pad": res.bad_pad, "first_bad_pad": res.first_bad_pad}
+
+
 def guard_workload(w, arena: np.ndarray) -> List[Dict]:
     """Guard and row-pad check of every allocation of w in `arena`."""
     out = []

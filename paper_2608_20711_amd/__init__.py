@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Sequence
+from typing import List, Optional, Sequence
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 # ASMEVO_LIBRARY may point at another build of the same library (tuning runs)
@@ -111,6 +111,11 @@ class GuardResult(ctypes.Structure):
                 ("bad_pad", ctypes.c_uint64), ("first_bad_pad", ctypes.c_int64)]
 
 
+class Kernel(ctypes.Structure):
+    _fields_ = [("module", ctypes.c_uint64), ("function", ctypes.c_uint64), ("num_regs", ctypes.c_int32),
+                ("shared_bytes", ctypes.c_int32), ("max_threads", ctypes.c_int32), ("local_bytes", ctypes.c_int32)]
+
+
 SEGMENT_RESULT_FIELDS = [f for f, _ in SegmentResult._fields_]
 GUARD_RESULT_FIELDS = [f for f, _ in GuardResult._fields_]
 
@@ -118,7 +123,8 @@ EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments
             "asmevo_diff_cosine", "asmevo_diff_cosine_workspace_bytes", "asmevo_copy_regions",
             "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
             "asmevo_abi_version", "asmevo_last_hip_error", "asmevo_diff_segments_nd",
-            "asmevo_diff_nd_workspace_bytes"]
+            "asmevo_diff_nd_workspace_bytes", "asmevo_kernel_load", "asmevo_kernel_unload",
+            "asmevo_kernel_launch", "asmevo_kernel_time"]
 
 
 class AsmevoError(RuntimeError):
@@ -164,6 +170,16 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_guard_check.restype = ctypes.c_int32
         L.asmevo_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int64]
         L.asmevo_workspace_bytes.restype = ctypes.c_size_t
+        L.asmevo_kernel_load.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_char_p, P(Kernel)]
+        L.asmevo_kernel_load.restype = ctypes.c_int32
+        L.asmevo_kernel_unload.argtypes = [P(Kernel)]
+        L.asmevo_kernel_unload.restype = ctypes.c_int32
+        u3 = ctypes.c_uint32 * 3
+        L.asmevo_kernel_launch.argtypes = [P(Kernel), u3, u3, ctypes.c_uint32, P(ctypes.c_void_p), vp]
+        L.asmevo_kernel_launch.restype = ctypes.c_int32
+        L.asmevo_kernel_time.argtypes = [P(Kernel), u3, u3, ctypes.c_uint32, P(ctypes.c_void_p), ctypes.c_int32,
+                                         ctypes.c_int32, P(ctypes.c_float), vp]
+        L.asmevo_kernel_time.restype = ctypes.c_int32
         L.asmevo_status_string.argtypes = [ctypes.c_int32]
         L.asmevo_status_string.restype = ctypes.c_char_p
         L.asmevo_abi_version.restype = ctypes.c_int32
@@ -268,3 +284,42 @@ def guard_check(allocs: Sequence[Alloc], seed: int, results_ptr: int, workspace_
     _check(_lib().asmevo_guard_check(a, len(allocs), seed, results_ptr, workspace_ptr,
                                      workspace_size, _stream_handle(stream)),
            "asmevo_guard_check")
+
+
+# --------------------------------------------------------------------------
+# code objects under test
+# --------------------------------------------------------------------------
+
+def kernel_load(image: bytes, name: str) -> Kernel:
+    k = Kernel()
+    _check(_lib().asmevo_kernel_load(image, len(image), name.encode(), ctypes.byref(k)), "asmevo_kernel_load")
+    return k
+
+
+def kernel_unload(k: Kernel) -> None:
+    _check(_lib().asmevo_kernel_unload(ctypes.byref(k)), "asmevo_kernel_unload")
+
+
+class KernelArgs:
+    """Explicit kernel arguments as ctypes values, kept alive with the
+    pointer array the runtime reads."""
+
+    def __init__(self, values: Sequence):
+        self.values = list(values)
+        self.params = (ctypes.c_void_p * max(1, len(self.values)))(
+            *[ctypes.cast(ctypes.pointer(v), ctypes.c_void_p) for v in self.values])
+
+
+def kernel_launch(k: Kernel, grid, block, args: KernelArgs, lds_bytes: int = 0, stream=None) -> None:
+    u3 = ctypes.c_uint32 * 3
+    _check(_lib().asmevo_kernel_launch(ctypes.byref(k), u3(*grid), u3(*block), lds_bytes, args.params,
+                                       _stream_handle(stream)), "asmevo_kernel_launch")
+
+
+def kernel_time(k: Kernel, grid, block, args: KernelArgs, warmup: int, reps: int, lds_bytes: int = 0,
+                stream=None) -> List[float]:
+    u3 = ctypes.c_uint32 * 3
+    ms = (ctypes.c_float * reps)()
+    _check(_lib().asmevo_kernel_time(ctypes.byref(k), u3(*grid), u3(*block), lds_bytes, args.params, warmup, reps,
+                                     ms, _stream_handle(stream)), "asmevo_kernel_time")
+    return [float(v) for v in ms]

@@ -699,4 +699,109 @@ asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t
   return ASMEVO_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Code objects: the kernel under test and its candidates are built into code
+// objects and run under the same launch (section 3.7, Algorithm 1).
+asmevo_status asmevo_kernel_load(const void* image, size_t image_bytes, const char* name,
+                                 asmevo_kernel* out) {
+  if (!image || image_bytes == 0 || !name || !out) return ASMEVO_E_INVALID;
+  std::memset(out, 0, sizeof(*out));
+  hipModule_t mod = nullptr;
+  HIP_TRY(hipModuleLoadData(&mod, image));
+  hipFunction_t fn = nullptr;
+  hipError_t e = hipModuleGetFunction(&fn, mod, name);
+  if (e != hipSuccess) {
+    g_last_hip = (int32_t)e;
+    (void)hipModuleUnload(mod);
+    return ASMEVO_E_HIP;
+  }
+  int regs = 0, shared = 0, threads = 0, local = 0;
+  (void)hipFuncGetAttribute(&regs, HIP_FUNC_ATTRIBUTE_NUM_REGS, fn);
+  (void)hipFuncGetAttribute(&shared, HIP_FUNC_ATTRIBUTE_SHARED_SIZE_BYTES, fn);
+  (void)hipFuncGetAttribute(&threads, HIP_FUNC_ATTRIBUTE_MAX_THREADS_PER_BLOCK, fn);
+  (void)hipFuncGetAttribute(&local, HIP_FUNC_ATTRIBUTE_LOCAL_SIZE_BYTES, fn);
+  out->module = reinterpret_cast<uint64_t>(mod);
+  out->function = reinterpret_cast<uint64_t>(fn);
+  out->num_regs = regs;
+  out->shared_bytes = shared;
+  out->max_threads = threads;
+  out->local_bytes = local;
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_kernel_unload(asmevo_kernel* k) {
+  if (!k) return ASMEVO_E_INVALID;
+  if (k->module) HIP_TRY(hipModuleUnload(reinterpret_cast<hipModule_t>(k->module)));
+  k->module = 0;
+  k->function = 0;
+  return ASMEVO_OK;
+}
+
+namespace {
+asmevo_status check_launch(const asmevo_kernel* k, const uint32_t grid[3], const uint32_t block[3],
+                           void** params) {
+  if (!k || !k->function || !grid || !block || !params) return ASMEVO_E_INVALID;
+  for (int d = 0; d < 3; ++d)
+    if (grid[d] == 0 || block[d] == 0) return ASMEVO_E_INVALID;
+  const uint64_t threads = (uint64_t)block[0] * block[1] * block[2];
+  if (k->max_threads > 0 && threads > (uint64_t)k->max_threads) return ASMEVO_E_INVALID;
+  return ASMEVO_OK;
+}
+}  // namespace
+
+asmevo_status asmevo_kernel_launch(const asmevo_kernel* k, const uint32_t grid[3], const uint32_t block[3],
+                                   uint32_t lds_bytes, void** params, void* stream) {
+  asmevo_status st = check_launch(k, grid, block, params);
+  if (st != ASMEVO_OK) return st;
+  HIP_TRY(hipModuleLaunchKernel(reinterpret_cast<hipFunction_t>(k->function), grid[0], grid[1], grid[2],
+                                block[0], block[1], block[2], lds_bytes,
+                                reinterpret_cast<hipStream_t>(stream), params, nullptr));
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_kernel_time(const asmevo_kernel* k, const uint32_t grid[3], const uint32_t block[3],
+                                 uint32_t lds_bytes, void** params, int32_t warmup, int32_t reps,
+                                 float* ms_out, void* stream) {
+  asmevo_status st = check_launch(k, grid, block, params);
+  if (st != ASMEVO_OK) return st;
+  if (warmup < 0 || reps <= 0 || !ms_out) return ASMEVO_E_INVALID;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipFunction_t fn = reinterpret_cast<hipFunction_t>(k->function);
+  for (int32_t w = 0; w < warmup; ++w)
+    HIP_TRY(hipModuleLaunchKernel(fn, grid[0], grid[1], grid[2], block[0], block[1], block[2], lds_bytes, s,
+                                  params, nullptr));
+  std::vector<hipEvent_t> ev(2 * (size_t)reps, nullptr);
+  asmevo_status result = ASMEVO_OK;
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) result = ASMEVO_E_HIP;
+  for (int32_t r = 0; r < reps && result == ASMEVO_OK; ++r) {
+    hipError_t e = hipEventRecord(ev[2 * r], s);
+    if (e == hipSuccess)
+      e = hipModuleLaunchKernel(fn, grid[0], grid[1], grid[2], block[0], block[1], block[2], lds_bytes, s,
+                                params, nullptr);
+    if (e == hipSuccess) e = hipEventRecord(ev[2 * r + 1], s);
+    if (e != hipSuccess) {
+      g_last_hip = (int32_t)e;
+      result = ASMEVO_E_HIP;
+    }
+  }
+  if (result == ASMEVO_OK) {
+    const hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+      g_last_hip = (int32_t)e;
+      result = ASMEVO_E_HIP;
+    }
+  }
+  for (int32_t r = 0; r < reps && result == ASMEVO_OK; ++r) {
+    const hipError_t e = hipEventElapsedTime(&ms_out[r], ev[2 * r], ev[2 * r + 1]);
+    if (e != hipSuccess) {
+      g_last_hip = (int32_t)e;
+      result = ASMEVO_E_HIP;
+    }
+  }
+  for (auto& e : ev)
+    if (e) (void)hipEventDestroy(e);
+  return result;
+}
+
 }  // extern "C"
