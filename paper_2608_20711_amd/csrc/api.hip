@@ -490,16 +490,43 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
 }
 
 // Cosine workspace: descriptors | one non-finite pair counter per segment |
-// three doubles per tile.
-struct CosLayout {
-  size_t off_counters, off_partials, bytes;
+// three doubles per tile | three doubles per level entry of the block trees |
+// CosLevels per segment | for each level k >= 1, n + 1 group prefix counts.
+struct CosPlan {
+  size_t off_counters = 0, off_partials = 0, off_levels = 0, off_lv = 0, off_prefix = 0, bytes = 0;
+  std::vector<CosLevels> lv;
+  std::vector<uint64_t> prefix;         // (kCosLevels - 1) x (n + 1)
+  uint64_t groups[kCosLevels] = {};     // groups per level (index 0 unused)
 };
-CosLayout cos_layout(int32_t n, uint64_t tiles) {
-  CosLayout L;
-  L.off_counters = align256((size_t)n * sizeof(DiffSeg));
-  L.off_partials = L.off_counters + align256((size_t)n * sizeof(uint64_t));
-  L.bytes = L.off_partials + (size_t)tiles * 3 * sizeof(double);
-  return L;
+
+CosPlan cos_plan(const std::vector<DiffSeg>& dev, uint64_t tiles) {
+  const size_t n = dev.size();
+  CosPlan P;
+  P.lv.assign(n, CosLevels{});
+  P.prefix.assign((size_t)(kCosLevels - 1) * (n + 1), 0);
+  uint64_t entries = 0;
+  for (size_t s = 0; s < n; ++s) {
+    CosLevels& L = P.lv[s];
+    L.off[0] = dev[s].tile_begin;
+    L.cnt[0] = is_float(dev[s].dtype) ? dev[s].tile_count : 0;   // integer segments store no block sums
+    for (int k = 1; k < kCosLevels; ++k) {
+      L.cnt[k] = L.cnt[k - 1] / 256;
+      L.off[k] = entries;
+      entries += L.cnt[k];
+    }
+  }
+  for (int k = 1; k < kCosLevels; ++k) {
+    uint64_t* pre = P.prefix.data() + (size_t)(k - 1) * (n + 1);
+    for (size_t s = 0; s < n; ++s) pre[s + 1] = pre[s] + P.lv[s].cnt[k];
+    P.groups[k] = pre[n];
+  }
+  P.off_counters = align256(n * sizeof(DiffSeg));
+  P.off_partials = P.off_counters + align256(n * sizeof(uint64_t));
+  P.off_levels = P.off_partials + align256((size_t)tiles * 3 * sizeof(double));
+  P.off_lv = P.off_levels + align256((size_t)entries * 3 * sizeof(double));
+  P.off_prefix = P.off_lv + align256(n * sizeof(CosLevels));
+  P.bytes = P.off_prefix + P.prefix.size() * sizeof(uint64_t);
+  return P;
 }
 
 }  // namespace
@@ -567,7 +594,7 @@ size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n)
   std::vector<DiffSeg> dev;
   uint64_t tiles = 0;
   if (n <= 0 || plan_diff(segs, n, true, dev, tiles) != ASMEVO_OK) return 0;
-  return cos_layout(n, tiles).bytes;
+  return cos_plan(dev, tiles).bytes;
 }
 
 asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
@@ -579,15 +606,24 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
   uint64_t tiles = 0;
   asmevo_status st = plan_diff(segs, n, true, dev, tiles);
   if (st != ASMEVO_OK) return st;
-  const CosLayout L = cos_layout(n, tiles);
-  if (!workspace || ws_bytes < L.bytes) return ASMEVO_E_WORKSPACE;
+  const CosPlan P = cos_plan(dev, tiles);
+  for (const CosLevels& L : P.lv)     // the final fold stages at most 255 entries per level
+    if (L.cnt[kCosLevels - 1] > 255) return ASMEVO_E_UNSUPPORTED;
+  if (!workspace || ws_bytes < P.bytes) return ASMEVO_E_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
   HIP_TRY(hipMemcpyAsync(ws, dev.data(), dev.size() * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
+  std::vector<uint8_t> tables(P.bytes - P.off_lv, 0);   // CosLevels | prefix counts, one upload
+  std::memcpy(tables.data(), P.lv.data(), P.lv.size() * sizeof(CosLevels));
+  std::memcpy(tables.data() + (P.off_prefix - P.off_lv), P.prefix.data(), P.prefix.size() * sizeof(uint64_t));
+  HIP_TRY(hipMemcpyAsync(ws + P.off_lv, tables.data(), tables.size(), hipMemcpyHostToDevice, s));
   const int wg = device_cus() * diff_blocks_per_cu();
   HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(ws), n, tiles, results, wg, s,
-                      reinterpret_cast<double*>(ws + L.off_partials),
-                      reinterpret_cast<unsigned long long*>(ws + L.off_counters), cos_results));
+                      reinterpret_cast<double*>(ws + P.off_partials),
+                      reinterpret_cast<unsigned long long*>(ws + P.off_counters), cos_results,
+                      reinterpret_cast<const CosLevels*>(ws + P.off_lv),
+                      reinterpret_cast<const uint64_t*>(ws + P.off_prefix), P.groups,
+                      reinterpret_cast<double*>(ws + P.off_levels)));
   return ASMEVO_OK;
 }
 

@@ -683,59 +683,32 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
   }
 }
 
-// One workgroup per segment: the left-complete pairwise tree over the
-// segment's block sums, as a binary counter -- aligned groups of 256 blocks
-// are perfect trees reduced in LDS, the remaining blocks are pushed one by
-// one; the counter's perfect trees, largest first, are then folded from the
-// right, which is exactly P(x[0..n)) = P(x[0..h)) + P(x[h..n)).
+// One level of the cosine's block tree: every workgroup reduces full aligned
+// groups of 256 level-(k-1) entries (perfect subtrees) to one level-k entry,
+// pairing neighbours level by level in LDS.  Groups are numbered across
+// segments by `prefix` (prefix[s] = the groups of segments before s).
 constexpr int kCosBlock = 256;
 
-__global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __restrict__ segs,
-                                                           const double* __restrict__ partials,
-                                                           const unsigned long long* nonfinite_pairs,
-                                                           asmevo_cosine_result* out) {
-  const int s = blockIdx.x;
-  const DiffSeg S = segs[s];
+__global__ __launch_bounds__(kCosBlock) void cos_level_kernel(const CosLevels* __restrict__ lv,
+                                                              const uint64_t* __restrict__ prefix, int n, int k,
+                                                              const double* __restrict__ partials,
+                                                              double* __restrict__ levels) {
   __shared__ double v[3][kCosBlock];
-  __shared__ double stack_val[3][64];
-  __shared__ int stack_lvl[64];
-  __shared__ int depth;
   const int t = threadIdx.x;
-  if (!(S.dtype >= ASMEVO_F32 && S.dtype <= ASMEVO_FP8_E4M3)) {
-    if (t == 0) {
-      asmevo_cosine_result r;
-      r.sum_ab = r.sum_aa = r.sum_bb = 0.0;
-      r.cosine = __builtin_nan("");
-      r.pairs = 0;
-      r.blocks = 0;
-      out[S.result_index] = r;
+  const uint64_t total = prefix[n];
+  for (uint64_t g = blockIdx.x; g < total; g += gridDim.x) {
+    int lo = 0, hi = n - 1;                  // last segment with prefix[s] <= g
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (prefix[mid] <= g) lo = mid;
+      else hi = mid - 1;
     }
-    return;
-  }
-  if (t == 0) depth = 0;
-  __syncthreads();
-  // push (value, level) onto the counter, merging equal levels (left + right)
-  auto push = [&](double ab, double aa, double bb, int lvl) {
-    while (depth > 0 && stack_lvl[depth - 1] == lvl) {
-      ab = stack_val[0][depth - 1] + ab;
-      aa = stack_val[1][depth - 1] + aa;
-      bb = stack_val[2][depth - 1] + bb;
-      --depth;
-      ++lvl;
-    }
-    stack_val[0][depth] = ab;
-    stack_val[1][depth] = aa;
-    stack_val[2][depth] = bb;
-    stack_lvl[depth] = lvl;
-    ++depth;
-  };
-  const uint64_t nb = S.tile_count;
-  const double* p = partials + 3 * S.tile_begin;
-  uint64_t g = 0;
-  for (; g + kCosBlock <= nb; g += kCosBlock) {
-    v[0][t] = p[3 * (g + t) + 0];
-    v[1][t] = p[3 * (g + t) + 1];
-    v[2][t] = p[3 * (g + t) + 2];
+    const uint64_t j = g - prefix[lo];
+    const CosLevels& L = lv[lo];
+    const double* src = (k == 1 ? partials + 3 * L.off[0] : levels + 3 * L.off[k - 1]) + 3 * (256 * j + t);
+    v[0][t] = src[0];
+    v[1][t] = src[1];
+    v[2][t] = src[2];
     __syncthreads();
     for (int width = kCosBlock / 2; width >= 1; width >>= 1) {
       double ab = 0.0, aa = 0.0, bb = 0.0;
@@ -752,38 +725,125 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
       }
       __syncthreads();
     }
-    if (t == 0) push(v[0][0], v[1][0], v[2][0], 8);
+    if (t == 0) {
+      double* dst = levels + 3 * (L.off[k] + j);
+      dst[0] = v[0][0];
+      dst[1] = v[1][0];
+      dst[2] = v[2][0];
+    }
     __syncthreads();
   }
-  if (t == 0) {
-    for (; g < nb; ++g) push(p[3 * g + 0], p[3 * g + 1], p[3 * g + 2], 0);
-    double ab = 0.0, aa = 0.0, bb = 0.0;
-    if (depth > 0) {
-      ab = stack_val[0][depth - 1];
-      aa = stack_val[1][depth - 1];
-      bb = stack_val[2][depth - 1];
-      for (int k = depth - 2; k >= 0; --k) {
-        ab = stack_val[0][k] + ab;
-        aa = stack_val[1][k] + aa;
-        bb = stack_val[2][k] + bb;
+}
+
+// One workgroup per segment.  The entries no level-k group absorbed (m_k <
+// 256 per level) are staged in LDS; their binary decomposition -- perfect
+// subtrees of sizes given by the set bits of m_k, largest first -- is
+// reduced in place in parallel (pairs 2^j apart inside every full aligned
+// block of 2^(j+1)).  One thread then pushes those subtree sums -- highest
+// level first, left to right -- onto a binary counter of perfect subtrees
+// (equal heights merge, left + right).  Folding the counter from the right
+// gives exactly the left-complete tree P(x[0..n)) = P(x[0..h)) + P(x[h..n))
+// over the segment's blocks.
+__global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __restrict__ segs,
+                                                           const CosLevels* __restrict__ lv,
+                                                           const double* __restrict__ partials,
+                                                           const double* __restrict__ levels,
+                                                           const unsigned long long* nonfinite_pairs,
+                                                           asmevo_cosine_result* out) {
+  constexpr int kLeft = 255;                       // at most 255 leftovers per level
+  __shared__ double left[3][kCosLevels * kLeft];
+  __shared__ double stack_val[3][64];
+  __shared__ int stack_lvl[64];
+  const int s = blockIdx.x;
+  const int t = threadIdx.x;
+  const DiffSeg S = segs[s];
+  if (!(S.dtype >= ASMEVO_F32 && S.dtype <= ASMEVO_FP8_E4M3)) {
+    if (t == 0) {
+      asmevo_cosine_result r;
+      r.sum_ab = r.sum_aa = r.sum_bb = 0.0;
+      r.cosine = __builtin_nan("");
+      r.pairs = 0;
+      r.blocks = 0;
+      out[S.result_index] = r;
+    }
+    return;
+  }
+  const CosLevels L = lv[s];
+  int m[kCosLevels];
+  for (int k = 0; k < kCosLevels; ++k) {
+    const uint64_t first = (k + 1 < kCosLevels) ? 256 * L.cnt[k + 1] : 0;
+    m[k] = (int)(L.cnt[k] - first);                // <= 255: first is cnt[k] rounded down to 256
+    const double* base = k == 0 ? partials + 3 * L.off[0] : levels + 3 * L.off[k];
+    for (int e = t; e < m[k]; e += kCosBlock) {
+      left[0][k * kLeft + e] = base[3 * (first + e) + 0];
+      left[1][k * kLeft + e] = base[3 * (first + e) + 1];
+      left[2][k * kLeft + e] = base[3 * (first + e) + 2];
+    }
+  }
+  __syncthreads();
+  for (int j = 0; j < 8; ++j) {
+    const int half = 1 << j, span = 2 << j;
+    for (int k = 0; k < kCosLevels; ++k) {
+      const int p = t * span;
+      if (p + span <= m[k]) {
+        const int q = k * kLeft + p;
+        left[0][q] = left[0][q] + left[0][q + half];
+        left[1][q] = left[1][q] + left[1][q + half];
+        left[2][q] = left[2][q] + left[2][q + half];
       }
     }
-    asmevo_cosine_result r;
-    r.sum_ab = ab;
-    r.sum_aa = aa;
-    r.sum_bb = bb;
-    if (aa == 0.0 && bb == 0.0) r.cosine = 1.0;
-    else if (aa == 0.0 || bb == 0.0) r.cosine = 0.0;
-    else {
-      const double na = __builtin_sqrt(aa);
-      const double nbb = __builtin_sqrt(bb);
-      const double den = na * nbb;
-      r.cosine = ab / den;
-    }
-    r.pairs = S.rows * S.cols - nonfinite_pairs[S.result_index];
-    r.blocks = nb;
-    out[S.result_index] = r;
+    __syncthreads();
   }
+  if (t != 0) return;
+  asmevo_cosine_result r;
+  int depth = 0;
+  for (int k = kCosLevels - 1; k >= 0; --k) {
+    int pos = 0;
+    for (int bit = 7; bit >= 0; --bit) {
+      if (!((m[k] >> bit) & 1)) continue;
+      const int q = k * kLeft + pos;
+      pos += 1 << bit;
+      double ab = left[0][q], aa = left[1][q], bb = left[2][q];
+      int lvl = 8 * k + bit;
+      while (depth > 0 && stack_lvl[depth - 1] == lvl) {
+        ab = stack_val[0][depth - 1] + ab;
+        aa = stack_val[1][depth - 1] + aa;
+        bb = stack_val[2][depth - 1] + bb;
+        --depth;
+        ++lvl;
+      }
+      stack_val[0][depth] = ab;
+      stack_val[1][depth] = aa;
+      stack_val[2][depth] = bb;
+      stack_lvl[depth] = lvl;
+      ++depth;
+    }
+  }
+  double ab = 0.0, aa = 0.0, bb = 0.0;
+  if (depth > 0) {
+    ab = stack_val[0][depth - 1];
+    aa = stack_val[1][depth - 1];
+    bb = stack_val[2][depth - 1];
+    for (int q = depth - 2; q >= 0; --q) {
+      ab = stack_val[0][q] + ab;
+      aa = stack_val[1][q] + aa;
+      bb = stack_val[2][q] + bb;
+    }
+  }
+  r.sum_ab = ab;
+  r.sum_aa = aa;
+  r.sum_bb = bb;
+  if (aa == 0.0 && bb == 0.0) r.cosine = 1.0;
+  else if (aa == 0.0 || bb == 0.0) r.cosine = 0.0;
+  else {
+    const double na = __builtin_sqrt(aa);
+    const double nbb = __builtin_sqrt(bb);
+    const double den = na * nbb;
+    r.cosine = ab / den;
+  }
+  r.pairs = S.rows * S.cols - nonfinite_pairs[S.result_index];
+  r.blocks = S.tile_count;
+  out[S.result_index] = r;
 }
 
 }  // namespace
@@ -809,7 +869,8 @@ int diff_nd_blocks_per_cu() {
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
                        double* partials, unsigned long long* nonfinite_pairs,
-                       asmevo_cosine_result* cos_results) {
+                       asmevo_cosine_result* cos_results, const CosLevels* levels_of,
+                       const uint64_t* level_prefix, const uint64_t* level_groups, double* levels) {
   if (n == 0) return hipSuccess;
   const bool cos = cos_results != nullptr;
   hipLaunchKernelGGL(diff_init_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, results, n,
@@ -829,7 +890,16 @@ hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
     if (e != hipSuccess) return e;
   }
   if (cos) {
-    hipLaunchKernelGGL(cosine_kernel, dim3(n), dim3(kCosBlock), 0, stream, segs, partials,
+    // levels 1.. of every segment's block tree, in parallel, then the per-segment fold
+    for (int k = 1; k < kCosLevels; ++k) {
+      if (level_groups[k] == 0) break;
+      const uint64_t grid = level_groups[k] < 65536 ? level_groups[k] : 65536;
+      hipLaunchKernelGGL(cos_level_kernel, dim3((unsigned)grid), dim3(kCosBlock), 0, stream, levels_of,
+                         level_prefix + (size_t)(k - 1) * (n + 1), n, k, partials, levels);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(cosine_kernel, dim3(n), dim3(kCosBlock), 0, stream, segs, levels_of, partials, levels,
                        nonfinite_pairs, cos_results);
     e = hipGetLastError();
   }

@@ -16,11 +16,17 @@ hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_p
 // Resident diff workgroups per compute unit (from the occupancy calculator).
 int diff_blocks_per_cu();
 // Diff of all segments; with cos_results, also the cosine term (partials:
-// three doubles per tile; nonfinite_pairs: one counter per segment).
+// three doubles per tile; nonfinite_pairs: one counter per segment; the
+// block tree by levels: levels_of[n] (device), level_prefix[(kCosLevels-1)
+// x (n+1)] (device: groups of the segments before s, per level),
+// level_groups[kCosLevels] (host: groups per level), levels: 3 doubles per
+// level entry).
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
                        double* partials = nullptr, unsigned long long* nonfinite_pairs = nullptr,
-                       asmevo_cosine_result* cos_results = nullptr);
+                       asmevo_cosine_result* cos_results = nullptr, const CosLevels* levels_of = nullptr,
+                       const uint64_t* level_prefix = nullptr, const uint64_t* level_groups = nullptr,
+                       double* levels = nullptr);
 
 // Resident N-D diff workgroups per compute unit.
 int diff_nd_blocks_per_cu();

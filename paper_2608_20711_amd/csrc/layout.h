@@ -85,6 +85,19 @@ struct NdExt {                  // 328 bytes
 };
 static_assert(sizeof(NdExt) == 328, "NdExt layout");
 
+// The cosine's block tree per segment, by levels: level 0 holds the block
+// sums (cnt[0] = the segment's tiles, at partials + 3 * off[0]); level k >= 1
+// holds one sum per full aligned group of 256 level-(k-1) entries (cnt[k] =
+// cnt[k-1] / 256, at levels + 3 * off[k]).  Such a group is a perfect
+// subtree of the left-complete tree, so the levels are reduced in parallel
+// and only the entries no group absorbed are folded per segment.
+constexpr int kCosLevels = 6;
+struct CosLevels {              // 96 bytes
+  uint64_t off[kCosLevels];
+  uint64_t cnt[kCosLevels];
+};
+static_assert(sizeof(CosLevels) == 96, "CosLevels layout");
+
 // ---------------------------------------------------------------- fill
 constexpr int kMaxRules = 16;      // Bernoulli rules per allocation
 constexpr int kFillBlock = 256;

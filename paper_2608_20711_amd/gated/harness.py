@@ -65,10 +65,12 @@ class Outcome:
     cv: Optional[float] = None
     checks: List[Dict] = field(default_factory=list)    # per (input, repeat) equivalence records
     static: List[str] = field(default_factory=list)     # failed static checks
+    wall_s: Optional[float] = None                      # host wall time of the whole evaluation
 
     def as_dict(self) -> Dict:
         return {"status": self.status, "reason": self.reason, "speedup": self.speedup, "t_k0_ms": self.t_k0_ms,
-                "t_ms": self.t_ms, "cv": self.cv, "static": self.static, "checks": self.checks}
+                "t_ms": self.t_ms, "cv": self.cv, "static": self.static, "checks": self.checks,
+                "wall_s": self.wall_s}
 
 
 def commit_gate(eq_all: bool, s_c: float, s_best: float, cv: float, eps: float = EPSILON, k: float = K_CV,
@@ -339,11 +341,14 @@ def search(harness: GatedEval, candidates) -> Tuple[List[Node], List[Tuple[str, 
     is committed when Eq. 2 holds against the current best K*.  Returns the
     lineage (committed nodes, K0 first) and (name, outcome, committed, bar)
     per candidate."""
+    import time
     lineage = [Node(0, "K0", None, 1.0)]
     best = lineage[0]
     log = []
     for cand in candidates:
+        t0 = time.perf_counter()
         out = harness.evaluate(cand.make(harness.s_k0, harness.s_k1))
+        out.wall_s = time.perf_counter() - t0
         committed, bar = False, None
         if out.status == "ok":
             committed, bar = commit_gate(True, out.speedup, best.speedup, out.cv)
@@ -353,3 +358,41 @@ def search(harness: GatedEval, candidates) -> Tuple[List[Node], List[Tuple[str, 
                 best = node
         log.append((cand.name, out, committed, bar))
     return lineage, log
+
+
+def main(argv=None) -> int:
+    """Runs the fixed candidates through GatedEval and the commit gate and
+    prints one JSON line: per-candidate outcome, speedup, threshold, commit,
+    wall time, and the lineage."""
+    import argparse
+    import json
+    import time
+    from .candidates import CANDIDATES
+    p = argparse.ArgumentParser(description=main.__doc__)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--reps", type=int, default=20)
+    args = p.parse_args(argv)
+    t0 = time.perf_counter()
+    h = GatedEval(warmup=args.warmup, reps=args.reps)
+    setup_s = time.perf_counter() - t0
+    try:
+        lineage, records = search(h, CANDIDATES)
+    finally:
+        h.close()
+    out = {"setup_s": round(setup_s, 3), "inputs": [x.spec.name for x in h.inputs],
+           "candidates": [{"name": n, "status": o.status, "reason": o.reason[:160],
+                           "speedup": None if o.speedup is None else round(o.speedup, 4),
+                           "t_k0_ms": None if o.t_k0_ms is None else round(o.t_k0_ms, 4),
+                           "t_ms": None if o.t_ms is None else round(o.t_ms, 4),
+                           "cv": None if o.cv is None else round(o.cv, 5),
+                           "bar": None if bar is None else round(bar, 5), "committed": c,
+                           "equivalence_checks": len(o.checks), "wall_s": round(o.wall_s, 3)}
+                          for n, o, c, bar in records],
+           "lineage": [{"id": nd.id, "name": nd.name, "parent": nd.parent, "speedup": round(nd.speedup, 4)}
+                       for nd in lineage]}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())

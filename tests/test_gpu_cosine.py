@@ -118,3 +118,29 @@ def test_cosine_every_fp8_and_f16_value():
         got = _cos_gpu(specs, a_d, b_d)
         want = [oracle.cosine_segment(dtype, 1, per, per, per, a_h, b_h, s["a_off"], s["b_off"]) for s in specs]
         assert_results_equal(got, want, f"{dtype} every value")
+
+
+def test_cosine_tree_levels_with_leftovers():
+    """Segments whose block counts leave entries at every level of the block
+    tree: 65536 + 5 * 256 + 3 blocks (one level-2 group, five level-1
+    groups, three single blocks), 3 * 256 + 255 and 257 blocks, and a 2-D
+    segment whose rows end in partial blocks."""
+    rng = np.random.default_rng(21)
+    n_blocks = 65536 + 5 * 256 + 3
+    n1 = n_blocks * 1024                                   # fp32: 1024 values per 4096-byte block
+    a = rng.standard_normal(n1 + 8192).astype(np.float32)
+    b = (a + rng.standard_normal(a.size).astype(np.float32) * 1e-3).astype(np.float32)
+    a_d = torch.from_numpy(a.view(np.uint8).copy()).cuda()
+    b_d = torch.from_numpy(b.view(np.uint8).copy()).cuda()
+    specs = [dict(dtype="f32", rows=1, cols=n1, sa=n1, sb=n1, a_off=0, b_off=0),
+             dict(dtype="f32", rows=1, cols=(3 * 256 + 255) * 1024, sa=1, sb=1, a_off=4096, b_off=4096),
+             dict(dtype="f32", rows=1, cols=257 * 1024 - 5, sa=1, sb=1, a_off=64, b_off=128),
+             dict(dtype="f32", rows=300, cols=1500, sa=1600, sb=1536, a_off=0, b_off=4)]
+    for s in specs:
+        s["sa"] = max(s["sa"], s["cols"])
+        s["sb"] = max(s["sb"], s["cols"])
+    got = _cos_gpu(specs, a_d, b_d)
+    want = [oracle.cosine_segment(s["dtype"], s["rows"], s["cols"], s["sa"], s["sb"], a.view(np.uint8),
+                                  b.view(np.uint8), s["a_off"], s["b_off"]) for s in specs]
+    assert_results_equal(got, want, "cosine tree levels")
+    assert got[0]["blocks"] == n_blocks
