@@ -55,7 +55,7 @@ def parse():
     p.add_argument("--workload", default="sweep")
     p.add_argument("--small", action="store_true", help="reduced-size workload (smoke runs)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-bytes", type=float, default=1.5 * 2 ** 30,
+    p.add_argument("--cpu-sample-bytes", type=float, default=32 * 2 ** 30,
                    help="logical bytes per side of the oracle's sample")
     p.add_argument("--workgroups", type=int, default=0)
     p.add_argument("--restore-steps", type=int, default=3,
