@@ -683,6 +683,7 @@ asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t
                                  asmevo_guard_result* results, void* workspace, size_t ws_bytes,
                                  void* stream) {
   if (n < 0 || (n > 0 && (!allocs || !results))) return ASMEVO_E_INVALID;
+  if (n > (1 << 29)) return ASMEVO_E_INVALID;   // result index and guard side share a 32-bit key
   if (n == 0) return ASMEVO_OK;
   std::vector<GuardRegion> regs;
   uint64_t chunks = 0;
