@@ -66,7 +66,8 @@ def parse():
                         "times on the last candidate and report it beside the metric (0: skip)")
     p.add_argument("--nd-steps", type=int, default=3,
                    help="after the timed steps, time N-D views of the two states (sliced rows, a "
-                        "permuted 4-D layout, a transposed matrix, a stride-2 gather, a block table)")
+                        "permuted 4-D layout, a transposed matrix, a stride-2 gather, narrow half rows, "
+                        "a block table)")
     p.add_argument("--read-probe", type=int, default=-1, metavar="GIB",
                    help="after the timed steps, run the two-stream HBM read probe over GIB per "
                         "side and report it as the measured read ceiling (-1: the workload's "
@@ -146,6 +147,7 @@ def nd_cases(st, stream, steps: int, scratch):
     if n >= m * 16:
         cases["transposed"] = [([n // m, m], [1, n // m], 0)]
     cases["stride2_gather"] = [([n // 2], [2], 0)]
+    cases["half_rows_256B"] = [([n // 128, 64], [128, 1], 0)]      # narrow rows: 256 of every 512 bytes
     blk = 1 << 19                                              # 2 MiB blocks
     if n >= 4 * blk:
         order = np.random.default_rng(7).permutation(n // blk).tolist()

@@ -445,16 +445,21 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
   }
 
   if (!kCos && (S.flags & kSegNarrow)) {
-    // Short rows: tiles over the row-major chunk space, each lane finds its row.
+    // Short rows: tiles over the row-major chunk space, each lane finds its
+    // row; all U chunk pairs of a tile are loaded before any is checked.
     const uint64_t total = S.rows * S.row_chunks;
     for (uint64_t tile = t_begin; tile < t_end; ++tile) {
       const uint64_t k0 = tile * (uint64_t)kTileChunks;
-#pragma unroll 1
+      u32x4 va[U], vb[U];
+      uint32_t nb[U];
+      uint64_t i0[U];
+#pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint64_t k = k0 + (uint64_t)(j * kWave) + lane;
-        u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
-        uint32_t nb = 0;
-        uint64_t i0 = 0;
+        va[j] = u32x4{0u, 0u, 0u, 0u};
+        vb[j] = u32x4{0u, 0u, 0u, 0u};
+        nb[j] = 0;
+        i0[j] = 0;
         if (k < total) {
           uint64_t r, c;
           if constexpr (ND) {
@@ -465,18 +470,20 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           }
           const uint64_t cb = c * kChunk;
           const uint64_t rem = S.row_bytes - cb;
-          nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+          nb[j] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
           if constexpr (ND) {
             uint64_t oa = 0, ob = 0;
             if (S.rows > 1) nd_row_offsets(X, r, oa, ob);   // a segment of several rows has an extension
-            load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb, vec, gather, in_sa, in_sb, va, vb);
+            load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb[j], vec, gather, in_sa, in_sb, va[j], vb[j]);
           } else {
-            load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb, vec, va, vb);
+            load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb[j], vec, va[j], vb[j]);
           }
-          i0 = ibase0 + r * S.cols + c * epc;
+          i0[j] = ibase0 + r * S.cols + c * epc;
         }
-        chunk<DT, ND>(va, vb, i0, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
       }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        chunk<DT, ND>(va[j], vb[j], i0[j], nb[j] / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
     }
     return;
   }
