@@ -545,7 +545,34 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       }
       continue;
     }
-    // Last tile of a row (or misaligned operands): per-chunk bounds.
+    // Last tile of a row (or misaligned operands): per-chunk bounds.  The
+    // plain diff issues all the tile's loads before checking any chunk (the
+    // latency of the row's last tile is then paid once); the cosine variant
+    // and N-D gathers, short of registers, go chunk by chunk.
+    if (!COS && !gather) {
+      u32x4 va[U], vb[U];
+      uint32_t nb[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+        va[j] = u32x4{0u, 0u, 0u, 0u};
+        vb[j] = u32x4{0u, 0u, 0u, 0u};
+        nb[j] = 0;
+        if (c < S.row_chunks) {
+          const uint64_t cb = c * kChunk;
+          const uint64_t rem = S.row_bytes - cb;
+          nb[j] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+          load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+        chunk<DT, ND>(va[j], vb[j], ibase + c * epc, nb[j] / es, tol_mode, strict, S.atol, S.rtol, acc, X,
+                      permuted);
+      }
+      continue;
+    }
 #pragma unroll 1
     for (int j = 0; j < U; ++j) {
       const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
