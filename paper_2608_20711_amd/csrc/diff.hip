@@ -7,8 +7,10 @@
 // Streaming, HBM-bound design for gfx950:
 //  * every segment is cut into tiles of 256 16-byte chunks (4 KiB per
 //    operand), each inside one row; all segments share one flat tile space;
-//  * each wave owns a contiguous range of tiles and issues 4 non-temporal
-//    dwordx4 loads per operand per lane before looking at any of them;
+//  * each wave owns a contiguous range of tiles (in the cosine variant the
+//    four waves of a workgroup share one range and take its tiles in turn)
+//    and issues 4 non-temporal dwordx4 loads per operand per lane before
+//    looking at any of them;
 //  * the common case is a 128-bit XOR that is zero: one combined check per
 //    tile, nothing else runs;
 //  * only chunks whose bits differ (or, under the strict NaN policy, hold a
@@ -19,9 +21,10 @@
 //    non-negative doubles as bit patterns), so results are identical for any
 //    schedule or launch geometry;
 //  * the cosine variant also accumulates fp64 a*b, a*a, b*b per lane over the
-//    same registers, folds each tile (= one 4096-byte block) with an xor
-//    butterfly and stores the block sums; cosine_kernel folds the blocks of a
-//    segment with the left-complete pairwise tree.
+//    same registers, folds each tile (= one 4096-byte block) with the xor
+//    butterfly's tree (permlane swaps and DPP) and stores the block sums;
+//    cos_level_kernel and cosine_kernel fold the blocks of a segment with the
+//    left-complete pairwise tree.
 #include "device_math.h"
 #include "kernels.h"
 #include "layout.h"
@@ -401,14 +404,54 @@ __device__ __forceinline__ void cos_chunk(const u32x4& va, const u32x4& vb, uint
   }
 }
 
-// Folds the lane sums of a block by the xor butterfly and stores them.
+// Lane i (< 32) receives v of lane i + 32 (v_permlane32_swap, gfx950).
+__device__ __forceinline__ double from_lane_plus32(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)u, (uint32_t)u, false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
+  return __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+}
+// Lane i (< 16) receives v of lane i + 16 (v_permlane16_swap, gfx950).
+__device__ __forceinline__ double from_lane_plus16(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)u, (uint32_t)u, false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
+  return __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+}
+// Lane i of each 16-lane row receives v of lane (i + 16 - R) mod 16 (DPP row_ror:R).
+template <int R>
+__device__ __forceinline__ double row_ror(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, 0x120 + R, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), 0x120 + R, 0xF, 0xF,
+                                                            false);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Folds the lane sums of a block and stores them from lane 0: the xor
+// butterfly's tree, lanes 32 apart first, then 16, 8, 4, 2, 1 (fp64 addition
+// commutes, so lane 0 of the butterfly adds exactly these pairs).  Lanes move
+// by permlane swaps and DPP rotations, without LDS; only lane 0's sums are
+// complete.  The whole wave must be active.
 __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    c.ab = c.ab + __shfl_xor(c.ab, m, kWave);
-    c.aa = c.aa + __shfl_xor(c.aa, m, kWave);
-    c.bb = c.bb + __shfl_xor(c.bb, m, kWave);
-  }
+  c.ab = c.ab + from_lane_plus32(c.ab);
+  c.aa = c.aa + from_lane_plus32(c.aa);
+  c.bb = c.bb + from_lane_plus32(c.bb);
+  c.ab = c.ab + from_lane_plus16(c.ab);
+  c.aa = c.aa + from_lane_plus16(c.aa);
+  c.bb = c.bb + from_lane_plus16(c.bb);
+  c.ab = c.ab + row_ror<8>(c.ab);
+  c.aa = c.aa + row_ror<8>(c.aa);
+  c.bb = c.bb + row_ror<8>(c.bb);
+  c.ab = c.ab + row_ror<12>(c.ab);
+  c.aa = c.aa + row_ror<12>(c.aa);
+  c.bb = c.bb + row_ror<12>(c.bb);
+  c.ab = c.ab + row_ror<14>(c.ab);
+  c.aa = c.aa + row_ror<14>(c.aa);
+  c.bb = c.bb + row_ror<14>(c.bb);
+  c.ab = c.ab + row_ror<15>(c.ab);
+  c.aa = c.aa + row_ror<15>(c.aa);
+  c.bb = c.bb + row_ror<15>(c.bb);
   if (lane == 0) {
     out[0] = c.ab;
     out[1] = c.aa;
@@ -421,7 +464,8 @@ __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
 // are placed by the segment's N-D extension X (the 2-D code otherwise).
 template <int DT, bool COS, bool ND>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
-                                           uint64_t t_end, uint32_t lane, Acc& acc, double* partials,
+                                           uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
+                                           double* partials,
                                            uint32_t& nonfinite) {
   constexpr int es = Et<DT>::es;
   constexpr int epc = 16 / es;
@@ -448,7 +492,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     // Short rows: tiles over the row-major chunk space, each lane finds its
     // row; all U chunk pairs of a tile are loaded before any is checked.
     const uint64_t total = S.rows * S.row_chunks;
-    for (uint64_t tile = t_begin; tile < t_end; ++tile) {
+    for (uint64_t tile = t_begin; tile < t_end; tile += step) {
       const uint64_t k0 = tile * (uint64_t)kTileChunks;
       u32x4 va[U], vb[U];
       uint32_t nb[U];
@@ -490,7 +534,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
 
   // Row-tiled: every tile lies inside one row (and is one cosine block).
   const uint64_t tpr = ND ? (S.row_chunks + kTileChunks - 1) / kTileChunks : (uint64_t)S.tiles_per_row;
-  for (uint64_t tile = t_begin; tile < t_end; ++tile) {
+  for (uint64_t tile = t_begin; tile < t_end; tile += step) {
     uint64_t r = 0, kt = tile;
     if (S.rows > 1) {
       if constexpr (ND) {
@@ -676,24 +720,29 @@ __attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU : ASMEVO_DIFF_W
 void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
                  uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                  unsigned long long* nonfinite_pairs) {
+  // kStep consecutive waves of a workgroup share one contiguous tile range
+  // and take its tiles in turn (kStep = 1: every wave has a range of its own).
+  constexpr uint32_t kStep = COS ? ASMEVO_COS_WAVE_STEP : ASMEVO_DIFF_WAVE_STEP;
+  static_assert(kStep >= 1 && (kDiffBlock / kWave) % kStep == 0, "a tile range stays inside a workgroup");
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = (uint64_t)blockIdx.x * (kDiffBlock / kWave) +
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const uint64_t nwaves = (uint64_t)gridDim.x * (kDiffBlock / kWave);
-  const uint64_t lo = total_tiles * wave / nwaves;
-  const uint64_t hi = total_tiles * (wave + 1) / nwaves;
-  if (lo >= hi) return;
-  int s_lo = 0, s_hi = n - 1;            // last segment with tile_begin <= lo
+  const uint64_t ngroups = (uint64_t)gridDim.x * (kDiffBlock / kWave) / kStep;
+  const uint64_t group = wave / kStep;
+  const uint64_t lo = total_tiles * group / ngroups;
+  const uint64_t hi = total_tiles * (group + 1) / ngroups;
+  uint64_t t = lo + wave % kStep;
+  if (t >= hi) return;
+  int s_lo = 0, s_hi = n - 1;            // last segment with tile_begin <= t
   while (s_lo < s_hi) {
     const int mid = (s_lo + s_hi + 1) >> 1;
-    if (segs[mid].tile_begin <= lo) s_lo = mid;
+    if (segs[mid].tile_begin <= t) s_lo = mid;
     else s_hi = mid - 1;
   }
   int s = s_lo;
   Acc acc;
   acc_reset(acc);
   uint32_t nonfinite = 0;
-  uint64_t t = lo;
   while (t < hi) {
     while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
     const DiffSeg S = segs[s];
@@ -702,18 +751,18 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
     const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
     const NdExt* X = (ND && S.nd_ext != ~0ull) ? ext + S.nd_ext : nullptr;
     switch (S.dtype) {
-      case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+      case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
       case ASMEVO_FP8_E4M3:
-        diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite);
+        diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
         break;
-      case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
-      case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
-      default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, lane, acc, partials, nonfinite); break;
+      case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+      case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+      default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
     }
     flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
-    t = t_end;
+    t += (t_end - t + kStep - 1) / kStep * kStep;     // this wave's first tile at or after t_end
   }
 }
 

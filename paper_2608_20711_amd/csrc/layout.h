@@ -13,14 +13,17 @@ constexpr int kChunk = 16;         // bytes per lane per load (dwordx4)
 #define ASMEVO_DIFF_UNROLL 4
 #endif
 constexpr int kDiffUnroll = ASMEVO_DIFF_UNROLL;      // chunks per lane per tile
-#ifndef ASMEVO_DIFF_PIPELINE                         // contiguous segments double-buffer tiles
-#define ASMEVO_DIFF_PIPELINE 0
-#endif
 #ifndef ASMEVO_DIFF_WAVES_PER_EU                     // occupancy target of the diff kernel
 #define ASMEVO_DIFF_WAVES_PER_EU 4
 #endif
 #ifndef ASMEVO_COS_WAVES_PER_EU                      // ... and of its cosine variant
 #define ASMEVO_COS_WAVES_PER_EU 3
+#endif
+#ifndef ASMEVO_DIFF_WAVE_STEP                        // waves of a workgroup sharing one tile range
+#define ASMEVO_DIFF_WAVE_STEP 1
+#endif
+#ifndef ASMEVO_COS_WAVE_STEP                         // ... in the cosine variant (4 resident
+#define ASMEVO_COS_WAVE_STEP 4                       // workgroups per CU: 4x fewer read streams)
 #endif
 constexpr int kTileChunks = kWave * kDiffUnroll;     // 256 chunks = 4 KiB per operand
 constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
