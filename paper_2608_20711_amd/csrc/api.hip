@@ -620,7 +620,7 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
   std::memcpy(tables.data(), P.lv.data(), P.lv.size() * sizeof(CosLevels));
   std::memcpy(tables.data() + (P.off_prefix - P.off_lv), P.prefix.data(), P.prefix.size() * sizeof(uint64_t));
   HIP_TRY(hipMemcpyAsync(ws + P.off_lv, tables.data(), tables.size(), hipMemcpyHostToDevice, s));
-  const int wg = device_cus() * diff_blocks_per_cu();
+  const int wg = device_cus() * cos_blocks_per_cu();   // the resident set
   HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(ws), n, tiles, results, wg, s,
                       reinterpret_cast<double*>(ws + P.off_partials),
                       reinterpret_cast<unsigned long long*>(ws + P.off_counters), cos_results,

@@ -931,9 +931,9 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 
 }  // namespace
 
-int diff_blocks_per_cu() {
+int cos_blocks_per_cu() {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false, false>, kDiffBlock, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<true, false>, kDiffBlock, 0) !=
           hipSuccess ||
       blocks <= 0)
     blocks = 4;

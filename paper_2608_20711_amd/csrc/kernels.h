@@ -13,8 +13,9 @@ hipError_t launch_fill(const FillAlloc* allocs, int n, const FillRule* rules, ui
 hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_pts, uint64_t seed,
                          hipStream_t stream);
 
-// Resident diff workgroups per compute unit (from the occupancy calculator).
-int diff_blocks_per_cu();
+// Resident workgroups per compute unit of the diff's cosine variant (from the
+// occupancy calculator).
+int cos_blocks_per_cu();
 // Diff of all segments; with cos_results, also the cosine term (partials:
 // three doubles per tile; nonfinite_pairs: one counter per segment; the
 // block tree by levels: levels_of[n] (device), level_prefix[(kCosLevels-1)
