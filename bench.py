@@ -120,10 +120,36 @@ def cpu_baseline(w, st, results, sample_bytes: float):
     dt = time.perf_counter() - t0
     compared = 2 * acc
     parity = all(got[k] == results[k] for k in picked)
+    # one thread on the first buffers of the same sample, up to 1 GiB per side
+    one_keys, one_acc = [], 0
+    for k in picked:
+        nb = w.allocs[w.compares[k].alloc].data_bytes
+        if one_acc + nb <= 2 ** 30:
+            one_keys.append(k)
+            one_acc += nb
+    t1 = time.perf_counter()
+    for k in one_keys:
+        one(k)
+    dt1 = time.perf_counter() - t1
     return {"value": round(compared / dt / 1e9, 4), "unit": "GB/s", "cores": CPU_THREADS, "kind": "oracle",
             "sample": f"{len(picked)} of {len(w.compares)} buffers, {acc / 2**30:.2f} GiB per side "
                       f"({compared / 2**30:.2f} GiB compared), diff only, {dt:.2f} s wall",
-            "parity_with_gpu": bool(parity)}
+            "parity_with_gpu": bool(parity),
+            "one_thread": {"value": round(2 * one_acc / dt1 / 1e9, 4) if dt1 > 0 else None, "unit": "GB/s",
+                           "sample": f"{len(one_keys)} buffers, {one_acc / 2**30:.2f} GiB per side, "
+                                     f"{dt1:.2f} s wall"},
+            "nproc": os.cpu_count(), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def nd_cases(st, stream, steps: int, scratch):

@@ -1,7 +1,10 @@
 // api.hip -- the C ABI (include/asmevo.h): argument validation, planning of
 // the device descriptor tables, one host-to-device copy into the caller's
 // workspace, kernel launches.  Validation finishes before anything is
-// enqueued, so an argument error leaves the stream untouched.
+// enqueued, so an argument error leaves the stream untouched.  The tables are
+// built in pageable host vectors that die with the call: hipMemcpyAsync from
+// pageable memory is synchronous (HIP stages it through a pinned buffer before
+// returning), so the copy has its bytes by then.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -812,8 +815,14 @@ asmevo_status asmevo_kernel_time(const asmevo_kernel* k, const uint32_t grid[3],
                                   params, nullptr));
   std::vector<hipEvent_t> ev(2 * (size_t)reps, nullptr);
   asmevo_status result = ASMEVO_OK;
-  for (auto& e : ev)
-    if (hipEventCreate(&e) != hipSuccess) result = ASMEVO_E_HIP;
+  for (auto& e : ev) {
+    const hipError_t c = hipEventCreate(&e);
+    if (c != hipSuccess) {
+      e = nullptr;
+      g_last_hip = (int32_t)c;
+      result = ASMEVO_E_HIP;
+    }
+  }
   for (int32_t r = 0; r < reps && result == ASMEVO_OK; ++r) {
     hipError_t e = hipEventRecord(ev[2 * r], s);
     if (e == hipSuccess)
