@@ -325,7 +325,7 @@ typedef struct {
  * float segment, from the same single pass over the operands (a second, small
  * kernel folds the per-block sums).  `results` as for asmevo_diff_segments;
  * `cos_results[0..n)` device memory.  The workspace must hold
- * asmevo_diff_cosine_workspace_bytes(segs, n) bytes (it keeps 24 bytes per
+ * asmevo_diff_cosine_workspace_bytes(segs, n) bytes (it keeps 32 bytes per
  * 4096-byte block).  Errors as for asmevo_diff_segments.
  */
 asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,

@@ -493,8 +493,9 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
 }
 
 // Cosine workspace: descriptors | one non-finite pair counter per segment |
-// three doubles per tile | three doubles per level entry of the block trees |
-// CosLevels per segment | for each level k >= 1, n + 1 group prefix counts.
+// one block-sum record (kCosRec doubles) per tile | one record per level
+// entry of the block trees | CosLevels per segment | for each level k >= 1,
+// n + 1 group prefix counts.
 struct CosPlan {
   size_t off_counters = 0, off_partials = 0, off_levels = 0, off_lv = 0, off_prefix = 0, bytes = 0;
   std::vector<CosLevels> lv;
@@ -525,8 +526,8 @@ CosPlan cos_plan(const std::vector<DiffSeg>& dev, uint64_t tiles) {
   }
   P.off_counters = align256(n * sizeof(DiffSeg));
   P.off_partials = P.off_counters + align256(n * sizeof(uint64_t));
-  P.off_levels = P.off_partials + align256((size_t)tiles * 3 * sizeof(double));
-  P.off_lv = P.off_levels + align256((size_t)entries * 3 * sizeof(double));
+  P.off_levels = P.off_partials + align256((size_t)tiles * kCosRec * sizeof(double));
+  P.off_lv = P.off_levels + align256((size_t)entries * kCosRec * sizeof(double));
   P.off_prefix = P.off_lv + align256(n * sizeof(CosLevels));
   P.bytes = P.off_prefix + P.prefix.size() * sizeof(uint64_t);
   return P;

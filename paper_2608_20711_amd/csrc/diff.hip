@@ -418,21 +418,24 @@ __device__ __forceinline__ double from_lane_plus16(double v) {
   const auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
   return __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
 }
-// Lane i of each 16-lane row receives v of lane (i + 16 - R) mod 16 (DPP row_ror:R).
-template <int R>
-__device__ __forceinline__ double row_ror(double v) {
+// v moved across lanes by one DPP pattern (CTRL: the instruction's dpp_ctrl),
+// 32 bits at a time: row_ror:R (0x120 + R) gives lane i of each 16-lane row
+// the value of lane (i + 16 - R) mod 16; quad_perm 0x4E and 0xB1 give lane i
+// of each group of four the value of lane i ^ 2 and i ^ 1.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t u = (uint64_t)__double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, 0x120 + R, 0xF, 0xF, false);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), 0x120 + R, 0xF, 0xF,
-                                                            false);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// Folds the lane sums of a block and stores them from lane 0: the xor
+// Folds the lane sums of a block and stores its record out[0..3]: the xor
 // butterfly's tree, lanes 32 apart first, then 16, 8, 4, 2, 1 (fp64 addition
-// commutes, so lane 0 of the butterfly adds exactly these pairs).  Lanes move
-// by permlane swaps and DPP rotations, without LDS; only lane 0's sums are
-// complete.  The whole wave must be active.
+// commutes, so lanes 0-3 of the butterfly add exactly these pairs).  Lanes
+// move by permlane swaps and DPP, without LDS; only lanes 0-3 end with the
+// complete sums, and they write the record with one store.  The whole wave
+// must be active.
 __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
   c.ab = c.ab + from_lane_plus32(c.ab);
   c.aa = c.aa + from_lane_plus32(c.aa);
@@ -440,22 +443,24 @@ __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
   c.ab = c.ab + from_lane_plus16(c.ab);
   c.aa = c.aa + from_lane_plus16(c.aa);
   c.bb = c.bb + from_lane_plus16(c.bb);
-  c.ab = c.ab + row_ror<8>(c.ab);
-  c.aa = c.aa + row_ror<8>(c.aa);
-  c.bb = c.bb + row_ror<8>(c.bb);
-  c.ab = c.ab + row_ror<12>(c.ab);
-  c.aa = c.aa + row_ror<12>(c.aa);
-  c.bb = c.bb + row_ror<12>(c.bb);
-  c.ab = c.ab + row_ror<14>(c.ab);
-  c.aa = c.aa + row_ror<14>(c.aa);
-  c.bb = c.bb + row_ror<14>(c.bb);
-  c.ab = c.ab + row_ror<15>(c.ab);
-  c.aa = c.aa + row_ror<15>(c.aa);
-  c.bb = c.bb + row_ror<15>(c.bb);
-  if (lane == 0) {
-    out[0] = c.ab;
-    out[1] = c.aa;
-    out[2] = c.bb;
+  c.ab = c.ab + dpp_f64<0x128>(c.ab);      // row_ror:8: lanes 0-7 get i + 8
+  c.aa = c.aa + dpp_f64<0x128>(c.aa);
+  c.bb = c.bb + dpp_f64<0x128>(c.bb);
+  c.ab = c.ab + dpp_f64<0x12C>(c.ab);      // row_ror:12: lanes 0-3 get i + 4
+  c.aa = c.aa + dpp_f64<0x12C>(c.aa);
+  c.bb = c.bb + dpp_f64<0x12C>(c.bb);
+  c.ab = c.ab + dpp_f64<0x4E>(c.ab);       // quad_perm [2,3,0,1]
+  c.aa = c.aa + dpp_f64<0x4E>(c.aa);
+  c.bb = c.bb + dpp_f64<0x4E>(c.bb);
+  c.ab = c.ab + dpp_f64<0xB1>(c.ab);       // quad_perm [1,0,3,2]
+  c.aa = c.aa + dpp_f64<0xB1>(c.aa);
+  c.bb = c.bb + dpp_f64<0xB1>(c.bb);
+  if (lane < (uint32_t)kCosRec) {
+    double v = 0.0;
+    v = lane == 2 ? c.bb : v;
+    v = lane == 1 ? c.aa : v;
+    v = lane == 0 ? c.ab : v;
+    out[lane] = v;
   }
 }
 
@@ -582,10 +587,11 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         for (int j = 0; j < U; ++j) cos_chunk_fast<DT>(va[j], vb[j], cs);
         if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
           cs = Cos{0.0, 0.0, 0.0};                 // this lane met a NaN or Inf: redo with checks
-#pragma unroll 1
+          // (unrolled: a run-time index would move va and vb out of registers)
+#pragma unroll
           for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], epc, cs, nonfinite);
         }
-        cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);
+        cos_store(cs, partials + kCosRec * (S.tile_begin + tile), lane);
       }
       continue;
     }
@@ -632,7 +638,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       chunk<DT, ND>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
       if constexpr (kCos) cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
     }
-    if constexpr (kCos) cos_store(cs, partials + 3 * (S.tile_begin + tile), lane);
+    if constexpr (kCos) cos_store(cs, partials + kCosRec * (S.tile_begin + tile), lane);
   }
 }
 
@@ -788,7 +794,8 @@ __global__ __launch_bounds__(kCosBlock) void cos_level_kernel(const CosLevels* _
     }
     const uint64_t j = g - prefix[lo];
     const CosLevels& L = lv[lo];
-    const double* src = (k == 1 ? partials + 3 * L.off[0] : levels + 3 * L.off[k - 1]) + 3 * (256 * j + t);
+    const double* src =
+        (k == 1 ? partials + kCosRec * L.off[0] : levels + kCosRec * L.off[k - 1]) + kCosRec * (256 * j + t);
     v[0][t] = src[0];
     v[1][t] = src[1];
     v[2][t] = src[2];
@@ -808,11 +815,9 @@ __global__ __launch_bounds__(kCosBlock) void cos_level_kernel(const CosLevels* _
       }
       __syncthreads();
     }
-    if (t == 0) {
-      double* dst = levels + 3 * (L.off[k] + j);
-      dst[0] = v[0][0];
-      dst[1] = v[1][0];
-      dst[2] = v[2][0];
+    if (t < kCosRec) {   // one 32-byte record from four lanes
+      double* dst = levels + kCosRec * (L.off[k] + j);
+      dst[t] = t == 0 ? v[0][0] : t == 1 ? v[1][0] : t == 2 ? v[2][0] : 0.0;
     }
     __syncthreads();
   }
@@ -856,11 +861,11 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
   for (int k = 0; k < kCosLevels; ++k) {
     const uint64_t first = (k + 1 < kCosLevels) ? 256 * L.cnt[k + 1] : 0;
     m[k] = (int)(L.cnt[k] - first);                // <= 255: first is cnt[k] rounded down to 256
-    const double* base = k == 0 ? partials + 3 * L.off[0] : levels + 3 * L.off[k];
+    const double* base = k == 0 ? partials + kCosRec * L.off[0] : levels + kCosRec * L.off[k];
     for (int e = t; e < m[k]; e += kCosBlock) {
-      left[0][k * kLeft + e] = base[3 * (first + e) + 0];
-      left[1][k * kLeft + e] = base[3 * (first + e) + 1];
-      left[2][k * kLeft + e] = base[3 * (first + e) + 2];
+      left[0][k * kLeft + e] = base[kCosRec * (first + e) + 0];
+      left[1][k * kLeft + e] = base[kCosRec * (first + e) + 1];
+      left[2][k * kLeft + e] = base[kCosRec * (first + e) + 2];
     }
   }
   __syncthreads();

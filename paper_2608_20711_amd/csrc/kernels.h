@@ -17,11 +17,11 @@ hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_p
 // occupancy calculator).
 int cos_blocks_per_cu();
 // Diff of all segments; with cos_results, also the cosine term (partials:
-// three doubles per tile; nonfinite_pairs: one counter per segment; the
-// block tree by levels: levels_of[n] (device), level_prefix[(kCosLevels-1)
-// x (n+1)] (device: groups of the segments before s, per level),
-// level_groups[kCosLevels] (host: groups per level), levels: 3 doubles per
-// level entry).
+// one block-sum record of kCosRec doubles per tile; nonfinite_pairs: one
+// counter per segment; the block tree by levels: levels_of[n] (device),
+// level_prefix[(kCosLevels-1) x (n+1)] (device: groups of the segments
+// before s, per level), level_groups[kCosLevels] (host: groups per level),
+// levels: one record per level entry).
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
                        double* partials = nullptr, unsigned long long* nonfinite_pairs = nullptr,

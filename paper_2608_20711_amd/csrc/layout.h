@@ -89,12 +89,15 @@ struct NdExt {                  // 328 bytes
 static_assert(sizeof(NdExt) == 328, "NdExt layout");
 
 // The cosine's block tree per segment, by levels: level 0 holds the block
-// sums (cnt[0] = the segment's tiles, at partials + 3 * off[0]); level k >= 1
-// holds one sum per full aligned group of 256 level-(k-1) entries (cnt[k] =
-// cnt[k-1] / 256, at levels + 3 * off[k]).  Such a group is a perfect
+// sums (cnt[0] = the segment's tiles, at partials + kCosRec * off[0]); level
+// k >= 1 holds one sum per full aligned group of 256 level-(k-1) entries
+// (cnt[k] = cnt[k-1] / 256, at levels + kCosRec * off[k]).  Such a group is a perfect
 // subtree of the left-complete tree, so the levels are reduced in parallel
 // and only the entries no group absorbed are folded per segment.
 constexpr int kCosLevels = 6;
+// doubles per block-sum record: {sum a*b, sum a*a, sum b*b, 0}, 32 bytes, so
+// one store from four lanes writes a whole 32-byte memory sector
+constexpr int kCosRec = 4;
 struct CosLevels {              // 96 bytes
   uint64_t off[kCosLevels];
   uint64_t cnt[kCosLevels];

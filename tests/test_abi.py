@@ -184,8 +184,8 @@ def test_cosine_workspace_and_errors():
     L = lib.lib()
     segs = (lib.Segment * 2)(_seg(), _seg(rows=3, cols=1000, stride_a=1024, stride_b=1024))
     need = L.asmevo_diff_cosine_workspace_bytes(segs, 2)
-    # descriptors + counters + 3 doubles per 4096-byte block (1 + 3 blocks)
-    assert need >= 2 * 128 + 2 * 8 + 4 * 24
+    # descriptors + counters + a 32-byte record per 4096-byte block (1 + 3 blocks)
+    assert need >= 2 * 128 + 2 * 8 + 4 * 32
     bad = (lib.Segment * 1)(_seg(dtype=99))
     assert L.asmevo_diff_cosine_workspace_bytes(bad, 1) == 0
     with pytest.raises(lib.AsmevoError) as e:
