@@ -339,7 +339,7 @@ def main():
         restored_ok = st.seg_results() == results
         moved = sum(n for _, n in spans)
         med_r = statistics.median(rms)
-        restore = {"ms_median": round(med_r, 4), "bytes_per_side": moved,
+        restore = {"ms_median": round(med_r, 4), "ms_each": [round(x, 3) for x in rms], "bytes_per_side": moved,
                    "GBps_read_plus_write": round(2 * moved / (med_r * 1e-3) / 1e9, 2),
                    "pct_of_hbm_peak": round(100 * 2 * moved / (med_r * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
                    "diff_after_restore_identical": restored_ok,

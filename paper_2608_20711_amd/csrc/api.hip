@@ -681,7 +681,10 @@ asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n, void*
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_copy(reinterpret_cast<const CopyRegion*>(workspace), n, tiles, device_cus() * 4, s));
+  // two workgroups per CU, each streaming one range with its four waves: of
+  // 1-8 workgroups per CU and 1-4 waves per range, the fastest on the 64 GiB
+  // restore (by 2-9 %, on allocations where the copy is not bound elsewhere)
+  HIP_TRY(launch_copy(reinterpret_cast<const CopyRegion*>(workspace), n, tiles, device_cus() * 2, s));
   return ASMEVO_OK;
 }
 

@@ -3,10 +3,11 @@
 // captured dispatch with identical launch parameters and memory contents,
 // restored in place so that absolute pointers inside the state stay valid).
 //
-// All regions share one flat tile space of 4 KiB tiles; each wave owns a
-// contiguous range of tiles.  A region whose source and destination have the
-// same address phase modulo 16 is copied with 16-byte non-temporal loads and
-// stores after a byte-wise head; other regions are copied byte by byte.
+// All regions share one flat tile space of 4 KiB tiles; the four waves of a
+// workgroup share a contiguous range of tiles and take them in turn.  A
+// region whose source and destination have the same address phase modulo 16
+// is copied with 16-byte non-temporal loads and stores after a byte-wise
+// head; other regions are copied byte by byte.
 #include "device_math.h"
 #include "kernels.h"
 #include "layout.h"
@@ -18,6 +19,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kCopyBlock = 256;
 
+#ifndef ASMEVO_COPY_WAVE_STEP                        // waves of a workgroup sharing one tile range
+#define ASMEVO_COPY_WAVE_STEP 4
+#endif
 #ifndef ASMEVO_COPY_NT_LOAD
 #define ASMEVO_COPY_NT_LOAD 1
 #endif
@@ -32,21 +36,27 @@ __device__ __forceinline__ void copy_bytes(uint64_t dst, uint64_t src, uint64_t 
 
 __global__ __launch_bounds__(kCopyBlock) void copy_kernel(const CopyRegion* __restrict__ regs, int n,
                                                           uint64_t total_tiles) {
+  // kStep consecutive waves of a workgroup share one contiguous tile range
+  // and take its tiles in turn (kStep = 1: every wave has a range of its own).
+  constexpr uint32_t kStep = ASMEVO_COPY_WAVE_STEP;
+  static_assert(kStep >= 1 && (kCopyBlock / kWave) % kStep == 0, "a tile range stays inside a workgroup");
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = (uint64_t)blockIdx.x * (kCopyBlock / kWave) +
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const uint64_t nwaves = (uint64_t)gridDim.x * (kCopyBlock / kWave);
-  const uint64_t lo = total_tiles * wave / nwaves;
-  const uint64_t hi = total_tiles * (wave + 1) / nwaves;
-  if (lo >= hi) return;
-  int s_lo = 0, s_hi = n - 1;            // last region with tile_begin <= lo
+  const uint64_t ngroups = (uint64_t)gridDim.x * (kCopyBlock / kWave) / kStep;
+  const uint64_t group = wave / kStep;
+  const uint64_t lo = total_tiles * group / ngroups;
+  const uint64_t hi = total_tiles * (group + 1) / ngroups;
+  const uint64_t first = lo + wave % kStep;
+  if (first >= hi) return;
+  int s_lo = 0, s_hi = n - 1;            // last region with tile_begin <= first
   while (s_lo < s_hi) {
     const int mid = (s_lo + s_hi + 1) >> 1;
-    if (regs[mid].tile_begin <= lo) s_lo = mid;
+    if (regs[mid].tile_begin <= first) s_lo = mid;
     else s_hi = mid - 1;
   }
   int s = s_lo;
-  for (uint64_t t = lo; t < hi; ++t) {
+  for (uint64_t t = first; t < hi; t += kStep) {
     while (s + 1 < n && regs[s + 1].tile_begin <= t) ++s;
     const CopyRegion R = regs[s];
     const uint64_t tile = t - R.tile_begin;
