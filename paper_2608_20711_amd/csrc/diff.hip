@@ -271,12 +271,16 @@ __device__ __forceinline__ void nd_row_offsets(const NdExt* X, uint64_t r, uint6
   ob = 0;
   const int nd = (int)X->nouter;
 #pragma unroll 1
-  for (int d = nd - 1; d >= 0; --d) {
+  for (int d = nd - 1; d > 0; --d) {
     uint64_t q, idx;
     divmod(r, X->oshape[d], q, idx);
     oa += idx * X->opa[d];
     ob += idx * X->opb[d];
     r = q;
+  }
+  if (nd > 0) {                     // the outermost index is what remains (r < oshape[0])
+    oa += r * X->opa[0];
+    ob += r * X->opb[0];
   }
 }
 
@@ -495,13 +499,19 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
 
   if (!kCos && (S.flags & kSegNarrow)) {
     // Short rows: tiles over the row-major chunk space, each lane finds its
-    // row; all U chunk pairs of a tile are loaded before any is checked.
+    // row; all U chunk pairs of a tile are loaded before any is checked.  A
+    // lane divides once per tile (its first chunk) and steps its other chunks,
+    // 64 apart, by the quotient and remainder of 64 by the row's chunks.
     const uint64_t total = S.rows * S.row_chunks;
+    const uint64_t n_rc = S.row_chunks;
+    const uint64_t q64 = (uint64_t)kWave / n_rc, r64 = (uint64_t)kWave - q64 * n_rc;
     for (uint64_t tile = t_begin; tile < t_end; tile += step) {
       const uint64_t k0 = tile * (uint64_t)kTileChunks;
       u32x4 va[U], vb[U];
       uint32_t nb[U];
       uint64_t i0[U];
+      uint64_t r, c;
+      divmod(k0 + lane, n_rc, r, c);
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint64_t k = k0 + (uint64_t)(j * kWave) + lane;
@@ -509,14 +519,15 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         vb[j] = u32x4{0u, 0u, 0u, 0u};
         nb[j] = 0;
         i0[j] = 0;
-        if (k < total) {
-          uint64_t r, c;
-          if constexpr (ND) {
-            divmod(k, S.row_chunks, r, c);
-          } else {
-            r = k / S.row_chunks;
-            c = k - r * S.row_chunks;
+        if (j > 0) {                      // (r, c) of chunk k from those of k - 64
+          r += q64;
+          c += r64;
+          if (c >= n_rc) {
+            c -= n_rc;
+            r += 1;
           }
+        }
+        if (k < total) {
           const uint64_t cb = c * kChunk;
           const uint64_t rem = S.row_bytes - cb;
           nb[j] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
