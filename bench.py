@@ -313,8 +313,10 @@ def main():
         import paper_2608_20711_amd as lib
         backup = torch.empty_like(st.cand)
         spans = [(w.offsets[k], a.total_bytes) for k, a in enumerate(w.allocs)]
-        snap = [lib.Region(backup.data_ptr() + o, st.cand.data_ptr() + o, n) for o, n in spans]
-        rest = [lib.Region(st.cand.data_ptr() + o, backup.data_ptr() + o, n) for o, n in spans]
+        snap = lib.descriptor_array([lib.Region(backup.data_ptr() + o, st.cand.data_ptr() + o, n)
+                                     for o, n in spans])
+        rest = lib.descriptor_array([lib.Region(st.cand.data_ptr() + o, backup.data_ptr() + o, n)
+                                     for o, n in spans])
         rws = torch.empty(lib.workspace_bytes(len(spans)), dtype=torch.uint8, device="cuda:0")
         lib.copy_regions(snap, rws.data_ptr(), rws.numel(), stream)
         torch.cuda.synchronize()

@@ -13,8 +13,8 @@ import numpy as np
 import torch
 
 from . import (Alloc, DIST_CODE, DTYPE_CODE, FILL_SATURATE, Injection, KIND_CODE, MODE_CODE,
-               NAN_CODE, INJ_RATE, SIDE_CODE, Segment, diff_cosine, diff_cosine_workspace_bytes,
-               diff_segments, fill_guarded, guard_check, workspace_bytes)
+               NAN_CODE, INJ_RATE, SIDE_CODE, Segment, descriptor_array, diff_cosine,
+               diff_cosine_workspace_bytes, diff_segments, fill_guarded, guard_check, workspace_bytes)
 
 SEG_RESULT_DTYPE = np.dtype([("mismatches", "<u8"), ("first_mismatch", "<i8"),
                              ("bitwise_mismatches", "<u8"), ("first_bitwise", "<i8"),
@@ -38,6 +38,10 @@ def injection_structs(w) -> List[Injection]:
     return out
 
 
+def _packed(items: list):
+    return descriptor_array(items) if items else items
+
+
 class DeviceState:
     def __init__(self, w, device: str = "cuda"):
         self.w = w
@@ -51,10 +55,11 @@ class DeviceState:
                                    dtype=torch.uint8, device=self.device)
         self.guard_res = torch.empty(max(1, len(w.allocs)) * GUARD_RESULT_DTYPE.itemsize,
                                      dtype=torch.uint8, device=self.device)
-        self.inj = injection_structs(w)
-        self.allocs_ref = self._alloc_structs(self.ref)
-        self.allocs_cand = self._alloc_structs(self.cand)
-        self.segments = self._segment_structs()
+        # descriptors are packed into ctypes arrays once: every call passes them as they are
+        self.inj = _packed(injection_structs(w))
+        self.allocs_ref = _packed(self._alloc_structs(self.ref))
+        self.allocs_cand = _packed(self._alloc_structs(self.cand))
+        self.segments = _packed(self._segment_structs())
         self.cos_ws = None
         self.cos_res = torch.empty(max(1, len(w.compares)) * COS_RESULT_DTYPE.itemsize,
                                    dtype=torch.uint8, device=self.device)
