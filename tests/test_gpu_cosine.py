@@ -144,3 +144,35 @@ def test_cosine_tree_levels_with_leftovers():
                                   b.view(np.uint8), s["a_off"], s["b_off"]) for s in specs]
     assert_results_equal(got, want, "cosine tree levels")
     assert got[0]["blocks"] == n_blocks
+
+
+def test_cosine_many_small_segments_mixed_dtypes():
+    """Hundreds of segments of 1 element to 9 blocks, of four float dtypes and
+    int32, in one call: the four waves of a workgroup take the tiles of one
+    range in turn, so most ranges start and end inside segments and most
+    segments are shared by several waves.  Sums, cosine and pair counts equal
+    the oracle's; the diff results equal the plain diff's."""
+    rng = np.random.default_rng(99)
+    nbytes = 8 << 20
+    vals = (rng.standard_normal(nbytes // 4) * 2).astype(np.float32)
+    a_h = vals.view(np.uint8).copy()
+    b_h = a_h.copy()
+    flip = rng.integers(0, nbytes, size=2000)
+    a_h[flip] ^= 0x10
+    a_d, b_d = torch.from_numpy(a_h).cuda(), torch.from_numpy(b_h).cuda()
+    specs, off = [], 0
+    dtypes = ["f32", "bf16", "f16", "fp8e4m3", "i32"]
+    for k in range(700):
+        dt = dtypes[k % 5]
+        es = ESIZE[dt]
+        nb = int(rng.choice([es, 4096 - es, 4096, 4096 + es, 3 * 4096 + 16, 9 * 4096, int(rng.integers(1, 40000))]))
+        cols = max(1, nb // es)
+        if off + cols * es > nbytes:
+            off = 0
+        specs.append(dict(dtype=dt, rows=1, cols=cols, sa=cols, sb=cols, a_off=off, b_off=off))
+        off = (off + cols * es + 15) // 16 * 16
+    log(f"[cosine small] {len(specs)} segments")
+    got = _cos_gpu(specs, a_d, b_d)
+    want = [oracle.cosine_segment(s["dtype"], s["rows"], s["cols"], s["sa"], s["sb"], a_h, b_h, s["a_off"],
+                                  s["b_off"]) for s in specs]
+    assert_results_equal(got, want, "many small segments cosine")

@@ -253,3 +253,53 @@ def test_fill_geometry_distributions_and_injections():
     g = st.guard_results()
     assert g[0]["bad_lo"] == 3 and g[0]["first_bad_lo"] == 7 and g[0]["bad_hi"] == 40
     assert g[9]["bad_hi"] == 8 and g[9]["first_bad_hi"] == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "fp8e4m3", "i64"])
+def test_every_narrow_row_width(dtype):
+    """Rows under half a tile (1 to 127 chunks of 16 bytes, plus partial
+    chunks) take the narrow path, where a lane divides its chunk index by the
+    row's chunks once per tile and steps its other chunks 64 apart: every such
+    width, with 16-byte and odd pitches, as 2-D segments and as N-D views,
+    equals the oracle field for field, for several grid sizes."""
+    rng = np.random.default_rng(0x5EED + ESIZE[dtype])
+    es = ESIZE[dtype]
+    nbytes = 6 << 20
+    a_h, b_h = _random_pair(nbytes, dtype, rng, rate=0.01)
+    a_d = torch.from_numpy(a_h).cuda()
+    b_d = torch.from_numpy(b_h).cuda()
+    epc = 16 // es
+    specs, nd = [], []
+    off = 0
+    for chunks in list(range(1, 128)) + [129]:
+        for extra in (0, 1) if epc > 1 else (0,):            # whole chunks, or one element more
+            cols = chunks * epc + extra
+            pitch = cols + (epc if chunks % 3 else 1)       # 16-byte pitches, or odd ones
+            rows = 1 + (37 * chunks) % 11 + (3000 // chunks) % 40
+            ext = ((rows - 1) * pitch + cols) * es
+            if off + ext + 64 > nbytes:
+                off = 0
+            specs.append(_spec(dtype, rows, cols, pitch, pitch, off, off))
+            nd.append((rows, cols, pitch, off))
+            off += ((ext + 4095) // 4096) * 4096 // 3 * 2 // 16 * 16
+    log(f"[narrow] {dtype}: {len(specs)} 2-D segments")
+    got = _gpu_diff(specs, a_d, b_d)
+    want = _ora_diff(specs, a_h, b_h)
+    assert_results_equal(got, want, f"{dtype} narrow 2-D")
+    for wg in (1, 7, 300):
+        assert _gpu_diff(specs, a_d, b_d, workgroups=wg) == got
+    # the same rows as N-D views [rows, cols] / [pitch, 1]
+    segs = []
+    for k, (rows, cols, pitch, o) in enumerate(nd):
+        mode = "bitwise" if dtype in ("i32", "i64", "u8") else "tolerance"
+        segs.append(lib.segment_nd(a_d.data_ptr() + o, b_d.data_ptr() + o, lib.DTYPE_CODE[dtype],
+                                   lib.MODE_CODE[mode], lib.NAN_CODE["equal"], [rows, cols], [pitch, 1],
+                                   [pitch, 1], 1e-3, 1e-3, k, 0))
+    res = torch.empty(len(segs) * SEG_RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    ws_size = lib.diff_nd_workspace_bytes(len(segs))
+    ws = torch.empty(ws_size, dtype=torch.uint8, device="cuda")
+    lib.diff_segments_nd(segs, res.data_ptr(), len(segs), ws.data_ptr(), ws_size)
+    torch.cuda.synchronize()
+    raw = res.cpu().numpy().view(SEG_RESULT_DTYPE)
+    got_nd = [{f: raw[f][k].item() for f in SEG_RESULT_DTYPE.names} for k in range(len(segs))]
+    assert_results_equal(got_nd, want, f"{dtype} narrow N-D")
