@@ -468,7 +468,16 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     D.full_chunks = D.row_bytes / kChunk;
     const bool aligned = unit && S.a % 16 == 0 && S.b % 16 == 0 && pitches16;
     const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
+    // gathers of every other element: rows that start 16-byte aligned load whole 32-byte windows
+    bool pitches16a = true, pitches16b = true;
+    for (int d = 0; d + 1 < nm; ++d) {
+      pitches16a = pitches16a && X.opa[d] % 16 == 0;
+      pitches16b = pitches16b && X.opb[d] % 16 == 0;
+    }
+    const bool pair2a = !unit && inner.sa == 2 && S.a % 16 == 0 && pitches16a;
+    const bool pair2b = !unit && inner.sb == 2 && S.b % 16 == 0 && pitches16b;
     D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) | (unit ? 0u : kSegGather) |
+              (pair2a ? kSegPair2A : 0u) | (pair2b ? kSegPair2B : 0u) |
               (permuted ? kSegPermuted : 0u) |
               ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
     if (D.rows > 1 || !unit || permuted) {   // only these segments read an extension

@@ -238,16 +238,41 @@ __device__ __forceinline__ u32x4 load_elems_strided(const uint8_t* p, uint32_t n
   return u32x4{w[0], w[1], w[2], w[3]};
 }
 
-// Chunk c of a row of an N-D segment whose rows start at pa / pb.
+// A chunk of elements 2 apart: the 32 bytes at p (16-byte aligned) in two
+// vector loads, of which the even elements are kept, packed in order.
+template <int DT>
+__device__ __forceinline__ u32x4 load_pairs(const uint8_t* p) {
+  constexpr int es = Et<DT>::es;
+  const u32x4 v0 = ld_nt(p), v1 = ld_nt(p + 16);
+  if constexpr (es == 8) {
+    return u32x4{v0.x, v0.y, v1.x, v1.y};
+  } else if constexpr (es == 4) {
+    return u32x4{v0.x, v0.z, v1.x, v1.z};
+  } else {
+    // v_perm_b32 picks bytes of {hi word, lo word} = bytes 7..4, 3..0
+    constexpr uint32_t sel = es == 2 ? 0x05040100u : 0x06040200u;
+    return u32x4{__builtin_amdgcn_perm(v0.y, v0.x, sel), __builtin_amdgcn_perm(v0.w, v0.z, sel),
+                 __builtin_amdgcn_perm(v1.y, v1.x, sel), __builtin_amdgcn_perm(v1.w, v1.z, sel)};
+  }
+}
+
+// Chunk c of a row of an N-D segment whose rows start at pa / pb.  A gather
+// whose elements are 2 apart in an operand (pair2a / pair2b) loads that
+// operand's chunk as 32 contiguous bytes, unless it is the row's last chunk:
+// every other chunk is followed by another element of the same row, so the
+// 32 bytes end before it and stay inside the view.
 template <int DT>
 __device__ __forceinline__ void load_nd_chunk(const uint8_t* pa, const uint8_t* pb, uint64_t c,
                                               uint32_t nbytes, bool vec, bool gather, uint64_t in_sa,
-                                              uint64_t in_sb, u32x4& va, u32x4& vb) {
+                                              uint64_t in_sb, bool pair2a, bool pair2b, bool last,
+                                              u32x4& va, u32x4& vb) {
   if (gather) {
     constexpr int epc = 16 / Et<DT>::es;
     const uint32_t nv = nbytes / Et<DT>::es;
-    va = load_elems_strided<DT>(pa + c * epc * in_sa, nv, in_sa);
-    vb = load_elems_strided<DT>(pb + c * epc * in_sb, nv, in_sb);
+    if (pair2a && !last) va = load_pairs<DT>(pa + c * 2 * kChunk);
+    else va = load_elems_strided<DT>(pa + c * epc * in_sa, nv, in_sa);
+    if (pair2b && !last) vb = load_pairs<DT>(pb + c * 2 * kChunk);
+    else vb = load_elems_strided<DT>(pb + c * epc * in_sb, nv, in_sb);
   } else {
     load_chunk<DT>(pa + c * kChunk, pb + c * kChunk, nbytes, vec, va, vb);
   }
@@ -486,11 +511,13 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
   uint64_t ibase0 = 0, in_sa = 0, in_sb = 0;
-  bool gather = false, permuted = false;
+  bool gather = false, permuted = false, pair2a = false, pair2b = false;
   if constexpr (ND) {
     permuted = (S.flags & kSegPermuted) != 0;
     ibase0 = permuted ? 0 : S.nd_index_base;  // reordered: indices are mapped on a mismatch
     gather = (S.flags & kSegGather) != 0;
+    pair2a = (S.flags & kSegPair2A) != 0;
+    pair2b = (S.flags & kSegPair2B) != 0;
     if (X != nullptr) {
       in_sa = X->in_sa;
       in_sb = X->in_sb;
@@ -534,7 +561,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           if constexpr (ND) {
             uint64_t oa = 0, ob = 0;
             if (S.rows > 1) nd_row_offsets(X, r, oa, ob);   // a segment of several rows has an extension
-            load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb[j], vec, gather, in_sa, in_sb, va[j], vb[j]);
+            load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb[j], vec, gather, in_sa, in_sb, pair2a, pair2b,
+                              c + 1 == S.row_chunks, va[j], vb[j]);
           } else {
             load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb[j], vec, va[j], vb[j]);
           }
@@ -606,11 +634,13 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       }
       continue;
     }
-    // Last tile of a row (or misaligned operands): per-chunk bounds.  The
-    // plain diff issues all the tile's loads before checking any chunk (the
-    // latency of the row's last tile is then paid once); the cosine variant
-    // and N-D gathers, short of registers, go chunk by chunk.
-    if (!COS && !gather) {
+    // Last tile of a row, misaligned operands or a gather: per-chunk bounds.
+    // The plain and N-D diffs issue all the tile's loads before checking any
+    // chunk (the latency is then paid once per tile); the cosine variant,
+    // short of registers, goes chunk by chunk.
+    // (gathers of 1- and 2-byte elements load each element on its own, up
+    // to 16 loads per chunk and operand: those keep one chunk in flight)
+    if (!COS && (!gather || Et<DT>::es >= 4 || (pair2a && pair2b))) {
       u32x4 va[U], vb[U];
       uint32_t nb[U];
 #pragma unroll
@@ -623,7 +653,10 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           const uint64_t cb = c * kChunk;
           const uint64_t rem = S.row_bytes - cb;
           nb[j] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-          load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
+          if constexpr (ND)
+            load_nd_chunk<DT>(pa, pb, c, nb[j], vec, gather, in_sa, in_sb, pair2a, pair2b,
+                              c + 1 == S.row_chunks, va[j], vb[j]);
+          else load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
         }
       }
 #pragma unroll
@@ -643,7 +676,9 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         const uint64_t cb = c * kChunk;
         const uint64_t rem = S.row_bytes - cb;
         nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-        if constexpr (ND) load_nd_chunk<DT>(pa, pb, c, nb, vec, gather, in_sa, in_sb, va, vb);
+        if constexpr (ND)
+          load_nd_chunk<DT>(pa, pb, c, nb, vec, gather, in_sa, in_sb, pair2a, pair2b, c + 1 == S.row_chunks,
+                            va, vb);
         else load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
       }
       chunk<DT, ND>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);

@@ -34,6 +34,8 @@ enum : uint32_t {
   kSegNarrow = 8u,    // short 2-D rows: tiles run over the flattened chunk space
   kSegGather = 16u,   // N-D: the innermost dimension is not unit-stride in a or b
   kSegPermuted = 32u, // N-D: visited in memory order, not logical order (see NdExt)
+  kSegPair2A = 64u,   // N-D gather: a's elements are 2 apart and its rows start 16-byte aligned
+  kSegPair2B = 128u,  // ... the same for b
 };
 
 // A segment is either "row-tiled" (every tile lies inside one row: contiguous

@@ -160,3 +160,47 @@ def test_larger_sliced_tensor():
                    view_b=b.transpose(1, 0, 2)[:, :, :1024])]
     got, want = _run(specs, a, b)
     assert_results_equal(got, want, "large sliced")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "i64", "u8"])
+def test_every_other_element_views(dtype):
+    """Views that take every other element of the innermost dimension: an
+    operand whose rows start 16-byte aligned loads each chunk but the row's
+    last as 32 contiguous bytes and keeps the even elements; misaligned
+    operands, the last chunk of every row (partial or whole) and broadcast
+    rows take the element-by-element path.  Row lengths from 1 to 2049
+    elements, both operands or one of them aligned."""
+    rng = np.random.default_rng(15)
+    specs, tensors = [], []
+    for L in (2, 3, 31, 32, 33, 64, 65, 129, 1000, 4098):
+        rows = 2 + 3000 // L
+        shape = (rows, L)
+        if dtype in ("f32", "f16"):
+            b = rng.standard_normal(shape).astype(NP_T[dtype])
+        else:
+            b = rng.integers(0, 200, size=shape).astype(NP_T[dtype])
+        tensors.append((b, _perturbed(b, rng, frac=0.01)))
+    for k, (b, a) in enumerate(tensors):
+        views = [
+            lambda x: x[:, ::2],                                     # aligned rows if L * es % 16 == 0
+            lambda x: x[1:, ::2],                                    # from the second row
+            lambda x: x[:, 1::2],                                    # odd start: misaligned
+            lambda x: x.reshape(-1)[::2],                            # one long row
+            lambda x: x.reshape(-1)[: x.size - 3][::2],              # a ragged last chunk
+            lambda x: np.broadcast_to(x[:1, ::2], (4, (x.shape[1] + 1) // 2)),   # broadcast rows
+        ]
+        for j, v in enumerate(views):
+            specs.append(_spec(v(a), a, b, dtype, result=len(specs), index_base=j, view_b=v(b)))
+        # one operand aligned, the other not
+        specs.append(_spec(a[:, ::2][:, : (a.shape[1] - 1) // 2], a, b, dtype, result=len(specs),
+                           view_b=b[:, 1::2][:, : (b.shape[1] - 1) // 2]))
+    # each tensor is its own pair of buffers
+    got_all, want_all = [], []
+    per = len(specs) // len(tensors)
+    for k, (b, a) in enumerate(tensors):
+        part = [dict(s, result=i) for i, s in enumerate(specs[k * per:(k + 1) * per])]
+        got, want = _run(part, a, b)
+        got_all += got
+        want_all += want
+    assert_results_equal(got_all, want_all, f"{dtype} every other element")
+    assert any(w["mismatches"] for w in want_all)
