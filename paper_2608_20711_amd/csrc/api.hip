@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -68,11 +69,17 @@ asmevo_status check_alloc_geometry(const asmevo_alloc& A) {
   return ASMEVO_OK;
 }
 
+// Compute units of the current device, queried once per device.
 int device_cus() {
+  constexpr int kDevices = 64;
+  static std::atomic<int> known[kDevices];   // 0 until queried
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
+  const bool cached = dev >= 0 && dev < kDevices;
+  if (cached && (cus = known[dev].load(std::memory_order_relaxed)) > 0) return cus;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     return 256;
+  if (cached) known[dev].store(cus, std::memory_order_relaxed);
   return cus;
 }
 

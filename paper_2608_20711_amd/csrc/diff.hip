@@ -982,23 +982,22 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 
 }  // namespace
 
-int cos_blocks_per_cu() {
-  int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<true, false>, kDiffBlock, 0) !=
-          hipSuccess ||
-      blocks <= 0)
-    blocks = 4;
+// Resident workgroups per CU of a diff kernel (one code object: queried once).
+template <bool COS, bool ND>
+int resident_blocks() {
+  static const int blocks = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, diff_kernel<COS, ND>, kDiffBlock, 0) != hipSuccess ||
+        b <= 0)
+      b = 4;
+    return b;
+  }();
   return blocks;
 }
 
-int diff_nd_blocks_per_cu() {
-  int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, diff_kernel<false, true>, kDiffBlock, 0) !=
-          hipSuccess ||
-      blocks <= 0)
-    blocks = 4;
-  return blocks;
-}
+int cos_blocks_per_cu() { return resident_blocks<true, false>(); }
+
+int diff_nd_blocks_per_cu() { return resident_blocks<false, true>(); }
 
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
