@@ -270,7 +270,9 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
   const FillAlloc* d_allocs = reinterpret_cast<const FillAlloc*>(ws);
   const FillRule* d_rules = reinterpret_cast<const FillRule*>(ws + off_rules);
   const PointEntry* d_pts = reinterpret_cast<const PointEntry*>(ws + off_pts);
-  const uint64_t waves = std::max<uint64_t>(1, std::min<uint64_t>(tiles, (uint64_t)device_cus() * 32));
+  // the resident grid, no more: every wave deals itself tiles to the end
+  const uint64_t resident = (uint64_t)device_cus() * fill_blocks_per_cu() * (kFillBlock / kWave);
+  const uint64_t waves = std::max<uint64_t>(1, std::min<uint64_t>(tiles, resident));
   const int wg = (int)((waves + (kFillBlock / kWave) - 1) / (kFillBlock / kWave));
   HIP_TRY(launch_fill(d_allocs, n, d_rules, tiles, seed, wg, s));
   HIP_TRY(launch_inject(d_allocs, d_pts, (int)points.size(), seed, s));

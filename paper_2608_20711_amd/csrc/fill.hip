@@ -416,8 +416,11 @@ __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillRul
   }
 }
 
-// Each wave walks a contiguous range of 64-chunk tiles (one chunk per lane);
-// tiles never straddle allocations.
+// Tiles of 64 chunks (one chunk per lane) never straddle allocations.  The
+// fill is bound by its arithmetic, whose cost per tile depends on the
+// element type (a tile of fp8 values draws 4x the normals of an fp32 one),
+// so the waves of the resident grid deal the tiles round-robin: every wave
+// gets the same mix and all finish together.
 __global__ __launch_bounds__(kFillBlock) void fill_kernel(const FillAlloc* __restrict__ allocs,
                                                           int n, const FillRule* __restrict__ rules,
                                                           uint64_t total_tiles, uint64_t seed) {
@@ -425,17 +428,15 @@ __global__ __launch_bounds__(kFillBlock) void fill_kernel(const FillAlloc* __res
   const uint64_t wave = (uint64_t)blockIdx.x * (kFillBlock / kWave) +
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const uint64_t nwaves = (uint64_t)gridDim.x * (kFillBlock / kWave);
-  const uint64_t lo = total_tiles * wave / nwaves;
-  const uint64_t hi = total_tiles * (wave + 1) / nwaves;
-  if (lo >= hi) return;
-  int s_lo = 0, s_hi = n - 1;             // last allocation with tile_begin <= lo
+  if (wave >= total_tiles) return;
+  int s_lo = 0, s_hi = n - 1;             // last allocation with tile_begin <= wave
   while (s_lo < s_hi) {
     const int mid = (s_lo + s_hi + 1) >> 1;
-    if (allocs[mid].tile_begin <= lo) s_lo = mid;
+    if (allocs[mid].tile_begin <= wave) s_lo = mid;
     else s_hi = mid - 1;
   }
   int k = s_lo;
-  for (uint64_t t = lo; t < hi; ++t) {
+  for (uint64_t t = wave; t < total_tiles; t += nwaves) {
     while (k + 1 < n && allocs[k + 1].tile_begin <= t) ++k;
     const FillAlloc A = allocs[k];
     const uint64_t o = ((t - A.tile_begin) * kWave + lane) * kChunk;
@@ -483,6 +484,16 @@ __global__ void inject_kernel(const FillAlloc* __restrict__ allocs,
 }
 
 }  // namespace
+
+int fill_blocks_per_cu() {
+  static const int blocks = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, fill_kernel, kFillBlock, 0) != hipSuccess || b <= 0)
+      b = 4;
+    return b;
+  }();
+  return blocks;
+}
 
 hipError_t launch_fill(const FillAlloc* allocs, int n, const FillRule* rules, uint64_t total_tiles,
                        uint64_t seed, int workgroups, hipStream_t stream) {

@@ -8,6 +8,8 @@
 
 namespace asmevo {
 
+// Resident fill workgroups per compute unit.
+int fill_blocks_per_cu();
 hipError_t launch_fill(const FillAlloc* allocs, int n, const FillRule* rules, uint64_t total_tiles,
                        uint64_t seed, int workgroups, hipStream_t stream);
 hipError_t launch_inject(const FillAlloc* allocs, const PointEntry* pts, int n_pts, uint64_t seed,
