@@ -8,9 +8,10 @@
 //  * every segment is cut into tiles of 256 16-byte chunks (4 KiB per
 //    operand), each inside one row; all segments share one flat tile space;
 //  * each wave owns a contiguous range of tiles (in the cosine variant the
-//    four waves of a workgroup share one range and take its tiles in turn)
-//    and issues 4 non-temporal dwordx4 loads per operand per lane before
-//    looking at any of them;
+//    four waves of a workgroup take the tiles of 1 MiB blocks in turn, the
+//    blocks dealt to the workgroups round-robin: the cosine's cost per tile
+//    depends on the element type) and issues 4 non-temporal dwordx4 loads
+//    per operand per lane before looking at any of them;
 //  * the common case is a 128-bit XOR that is zero: one combined check per
 //    tile, nothing else runs;
 //  * only chunks whose bits differ (or, under the strict NaN policy, hold a
@@ -772,49 +773,65 @@ __attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU : ASMEVO_DIFF_W
 void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
                  uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                  unsigned long long* nonfinite_pairs) {
-  // kStep consecutive waves of a workgroup share one contiguous tile range
-  // and take its tiles in turn (kStep = 1: every wave has a range of its own).
+  // kStep consecutive waves of a workgroup share their tiles and take them in
+  // turn (kStep = 1: every wave has tiles of its own).  With kDeal = 0 the
+  // group's tiles are one contiguous range; otherwise blocks of kDeal tiles
+  // are dealt to the groups round-robin, so every group sees the same mix
+  // of segments (and of element types).
   constexpr uint32_t kStep = COS ? ASMEVO_COS_WAVE_STEP : ASMEVO_DIFF_WAVE_STEP;
+  constexpr uint64_t kDeal = COS ? ASMEVO_COS_DEAL : ASMEVO_DIFF_DEAL;
   static_assert(kStep >= 1 && (kDiffBlock / kWave) % kStep == 0, "a tile range stays inside a workgroup");
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = (uint64_t)blockIdx.x * (kDiffBlock / kWave) +
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const uint64_t ngroups = (uint64_t)gridDim.x * (kDiffBlock / kWave) / kStep;
   const uint64_t group = wave / kStep;
-  const uint64_t lo = total_tiles * group / ngroups;
-  const uint64_t hi = total_tiles * (group + 1) / ngroups;
-  uint64_t t = lo + wave % kStep;
-  if (t >= hi) return;
-  int s_lo = 0, s_hi = n - 1;            // last segment with tile_begin <= t
-  while (s_lo < s_hi) {
-    const int mid = (s_lo + s_hi + 1) >> 1;
-    if (segs[mid].tile_begin <= t) s_lo = mid;
-    else s_hi = mid - 1;
-  }
-  int s = s_lo;
+  int s = -1;
   Acc acc;
   acc_reset(acc);
   uint32_t nonfinite = 0;
-  while (t < hi) {
-    while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
-    const DiffSeg S = segs[s];
-    const uint64_t seg_end = S.tile_begin + S.tile_count;
-    const uint64_t t_end = seg_end < hi ? seg_end : hi;
-    const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
-    const NdExt* X = (ND && S.nd_ext != ~0ull) ? ext + S.nd_ext : nullptr;
-    switch (S.dtype) {
-      case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-      case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-      case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-      case ASMEVO_FP8_E4M3:
-        diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
-        break;
-      case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-      case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-      default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+  for (uint64_t j = group;; j += ngroups) {
+    uint64_t lo, hi;
+    if constexpr (kDeal == 0) {
+      lo = total_tiles * group / ngroups;
+      hi = total_tiles * (group + 1) / ngroups;
+    } else {
+      lo = j * kDeal;
+      if (lo >= total_tiles) break;
+      hi = lo + kDeal < total_tiles ? lo + kDeal : total_tiles;
     }
-    flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
-    t += (t_end - t + kStep - 1) / kStep * kStep;     // this wave's first tile at or after t_end
+    uint64_t t = lo + wave % kStep;
+    if (t < hi && s < 0) {
+      int s_lo = 0, s_hi = n - 1;        // last segment with tile_begin <= t
+      while (s_lo < s_hi) {
+        const int mid = (s_lo + s_hi + 1) >> 1;
+        if (segs[mid].tile_begin <= t) s_lo = mid;
+        else s_hi = mid - 1;
+      }
+      s = s_lo;
+    }
+    while (t < hi) {
+      while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
+      const DiffSeg S = segs[s];
+      const uint64_t seg_end = S.tile_begin + S.tile_count;
+      const uint64_t t_end = seg_end < hi ? seg_end : hi;
+      const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
+      const NdExt* X = (ND && S.nd_ext != ~0ull) ? ext + S.nd_ext : nullptr;
+      switch (S.dtype) {
+        case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_FP8_E4M3:
+          diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
+          break;
+        case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+      }
+      flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
+      t += (t_end - t + kStep - 1) / kStep * kStep;   // this wave's first tile at or after t_end
+    }
+    if constexpr (kDeal == 0) break;
   }
 }
 

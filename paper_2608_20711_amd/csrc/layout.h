@@ -25,6 +25,12 @@ constexpr int kDiffUnroll = ASMEVO_DIFF_UNROLL;      // chunks per lane per tile
 #ifndef ASMEVO_COS_WAVE_STEP                         // ... in the cosine variant (4 resident
 #define ASMEVO_COS_WAVE_STEP 4                       // workgroups per CU: 4x fewer read streams)
 #endif
+#ifndef ASMEVO_DIFF_DEAL                             // tiles per block dealt round-robin (0: ranges)
+#define ASMEVO_DIFF_DEAL 0
+#endif
+#ifndef ASMEVO_COS_DEAL                              // ... in the cosine variant, whose cost per
+#define ASMEVO_COS_DEAL 256                          // tile depends on the element type
+#endif
 constexpr int kTileChunks = kWave * kDiffUnroll;     // 256 chunks = 4 KiB per operand
 constexpr int kDiffBlock = 256;                      // 4 waves per workgroup
 
