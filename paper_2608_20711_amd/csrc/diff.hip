@@ -776,8 +776,9 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
   // kStep consecutive waves of a workgroup share their tiles and take them in
   // turn (kStep = 1: every wave has tiles of its own).  With kDeal = 0 the
   // group's tiles are one contiguous range; otherwise blocks of kDeal tiles
-  // are dealt to the groups round-robin, so every group sees the same mix
-  // of segments (and of element types).
+  // (fewer when the groups would not all get one) are dealt to the groups
+  // round-robin, so every group sees the same mix of segments (and of
+  // element types).
   constexpr uint32_t kStep = COS ? ASMEVO_COS_WAVE_STEP : ASMEVO_DIFF_WAVE_STEP;
   constexpr uint64_t kDeal = COS ? ASMEVO_COS_DEAL : ASMEVO_DIFF_DEAL;
   static_assert(kStep >= 1 && (kDiffBlock / kWave) % kStep == 0, "a tile range stays inside a workgroup");
@@ -786,6 +787,8 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const uint64_t ngroups = (uint64_t)gridDim.x * (kDiffBlock / kWave) / kStep;
   const uint64_t group = wave / kStep;
+  const uint64_t per_group = (total_tiles + ngroups - 1) / ngroups;
+  const uint64_t block = kDeal < per_group ? kDeal : per_group;
   int s = -1;
   Acc acc;
   acc_reset(acc);
@@ -796,9 +799,9 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
       lo = total_tiles * group / ngroups;
       hi = total_tiles * (group + 1) / ngroups;
     } else {
-      lo = j * kDeal;
+      lo = j * block;
       if (lo >= total_tiles) break;
-      hi = lo + kDeal < total_tiles ? lo + kDeal : total_tiles;
+      hi = lo + block < total_tiles ? lo + block : total_tiles;
     }
     uint64_t t = lo + wave % kStep;
     if (t < hi && s < 0) {
