@@ -60,28 +60,20 @@ template <> struct Et<ASMEVO_I32> { static constexpr int es = 4; static constexp
 template <> struct Et<ASMEVO_I64> { static constexpr int es = 8; static constexpr bool fp = false; };
 template <> struct Et<ASMEVO_U8> { static constexpr int es = 1; static constexpr bool fp = false; };
 
-template <int DT>
-__device__ __forceinline__ uint64_t elem(const u32x4& v, int e) {
-  // e is a compile-time constant at every call of this form
-  constexpr int es = Et<DT>::es;
-  if constexpr (es == 4) return v[e];
-  else if constexpr (es == 2) return (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-  else if constexpr (es == 1) return (v[e >> 2] >> (8 * (e & 3))) & 0xFFu;
-  else return (uint64_t)v[2 * e] | ((uint64_t)v[2 * e + 1] << 32);
-}
-
 // Element e (a run-time value) of a chunk, selected without indexing into
 // registers (which would go through scratch memory).
 template <int DT>
 __device__ __forceinline__ uint64_t elem_dyn(const u32x4& v, uint32_t e) {
   constexpr uint32_t es = Et<DT>::es;
   const uint32_t byte = e * es;
-  const uint32_t wi = byte >> 2;
-  const uint32_t w = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
+  const bool odd = (byte & 4u) != 0, high = (byte & 8u) != 0;   // word = byte / 4
   if constexpr (es == 8) {
-    const uint32_t w2 = wi == 0 ? v.y : v.w;
+    const uint32_t w = high ? v.z : v.x;
+    const uint32_t w2 = high ? v.w : v.y;
     return (uint64_t)w | ((uint64_t)w2 << 32);
-  } else if constexpr (es == 4) {
+  }
+  const uint32_t w = high ? (odd ? v.w : v.z) : (odd ? v.y : v.x);
+  if constexpr (es == 4) {
     return w;
   } else {
     return (w >> (8u * (byte & 3u))) & ((1u << (8u * es)) - 1u);
@@ -97,48 +89,112 @@ __device__ __forceinline__ bool is_nan_raw(uint64_t r) {
   else return false;
 }
 
+// Exact fp64 value of an element given its raw bits (any value for Inf and
+// NaN, which the callers test for separately): binary32 and bfloat16 by a
+// bit cast, binary16 by v_cvt_f32_f16, fp8 e4m3 by v_cvt_f32_fp8 (both exact,
+// subnormals kept), then binary32 -> binary64, which is exact.
+template <int DT>
+__device__ __forceinline__ double raw_f64(uint32_t r) {
+  if constexpr (DT == ASMEVO_F32) return (double)__uint_as_float(r);
+  else if constexpr (DT == ASMEVO_BF16) return (double)__uint_as_float(r << 16);
+  else if constexpr (DT == ASMEVO_F16) return (double)(float)__builtin_bit_cast(_Float16, (uint16_t)r);
+  else return (double)__builtin_amdgcn_cvt_f32_fp8((int)r, 0);
+}
+
+template <int DT>
+__device__ __forceinline__ bool is_finite_raw(uint32_t r) {
+  if constexpr (DT == ASMEVO_F32) return (r & 0x7F800000u) != 0x7F800000u;
+  else if constexpr (DT == ASMEVO_BF16) return (r & 0x7F80u) != 0x7F80u;
+  else if constexpr (DT == ASMEVO_F16) return (r & 0x7C00u) != 0x7C00u;
+  else return (r & 0x7Fu) != 0x7Fu;       // e4m3fn: no infinities, S.1111.111 is NaN
+}
+
 // One element pair that needs attention: bits differ, or b is a NaN under the
-// strict policy.  Implements the per-pair rule of the tolerance check.
+// strict policy.  Implements the per-pair rule of the tolerance check.  The
+// rule is evaluated without branches (every quantity is computed and the
+// outcome selected), so lanes of a wave that hold different cases run it
+// together.
 template <int DT>
 __device__ __forceinline__ void pair_slow(uint64_t ra, uint64_t rb, uint64_t i, bool tol_mode,
                                        bool strict, double atol, double rtol, Acc& acc) {
   const bool bw = ra != rb;
-  if (bw) {
-    acc.bw += 1;
-    acc.first_bw = i < acc.first_bw ? i : acc.first_bw;
-  }
+  acc.bw += bw ? 1u : 0u;
+  acc.first_bw = (bw && i < acc.first_bw) ? i : acc.first_bw;
   if constexpr (Et<DT>::fp) {
-    if (!tol_mode) return;
-    double A = 0.0, B = 0.0;
-    const int ca = decode<DT>(ra, A);
-    const int cb = decode<DT>(rb, B);
-    const bool nonfinite = (ca | cb) != 0;
-    bool mism;
-    if (!bw) {
-      mism = (cb == 3) && strict;
-    } else if (ca == 3 || cb == 3) {
-      mism = !(ca == 3 && cb == 3 && !strict);
-    } else if (nonfinite) {
-      mism = true;
-    } else {
-      const double d = __builtin_fabs(A - B);
-      const double scaled = rtol * __builtin_fabs(B);
-      const double t = atol + scaled;
-      mism = !(d <= t);
-      double rel;
-      if (B != 0.0) rel = d / __builtin_fabs(B);
-      else rel = (d == 0.0) ? 0.0 : __builtin_inf();
-      const uint64_t db = (uint64_t)__double_as_longlong(d);
-      const uint64_t rb_ = (uint64_t)__double_as_longlong(rel);
-      acc.max_abs = db > acc.max_abs ? db : acc.max_abs;
-      acc.max_rel = rb_ > acc.max_rel ? rb_ : acc.max_rel;
+    if (!tol_mode) return;                  // uniform across the wave
+    const uint32_t xa = (uint32_t)ra, xb = (uint32_t)rb;
+    const bool nan_a = is_nan_raw<DT>(xa), nan_b = is_nan_raw<DT>(xb);
+    const bool finite = is_finite_raw<DT>(xa) && is_finite_raw<DT>(xb);
+    const double A = raw_f64<DT>(xa), B = raw_f64<DT>(xb);
+    const double d = __builtin_fabs(A - B);
+    const double mag_b = __builtin_fabs(B);
+    const double scaled = rtol * mag_b;
+    const double t = atol + scaled;
+    // bits equal: only a NaN under the strict policy fails; a NaN on either
+    // side fails unless both are NaN and the policy is EQUAL; an Inf whose
+    // bits differ fails; finite values fail the tolerance test
+    // (as 0/1 words combined with bitwise operators, which keeps the
+    // compiler from turning the cases into branches)
+    const uint32_t w_bw = bw, w_na = nan_a, w_nb = nan_b, w_st = strict;
+    const uint32_t w_fail = (uint32_t)(!finite) | (uint32_t)!(d <= t);
+    const uint32_t w_nan = w_na | w_nb;
+    const bool mism = ((~w_bw & w_nb & w_st) | (w_bw & w_nan & ~(w_na & w_nb & ~w_st)) |
+                       (w_bw & ~w_nan & w_fail)) & 1u;
+    const double q = d / mag_b;
+    const double rel = mag_b != 0.0 ? q : (d == 0.0 ? 0.0 : __builtin_inf());
+    const bool upd = bw && finite;          // the maxima cover finite pairs whose bits differ
+    const uint64_t db = upd ? (uint64_t)__double_as_longlong(d) : 0ull;
+    const uint64_t rlb = upd ? (uint64_t)__double_as_longlong(rel) : 0ull;
+    acc.max_abs = db > acc.max_abs ? db : acc.max_abs;
+    acc.max_rel = rlb > acc.max_rel ? rlb : acc.max_rel;
+    acc.tol += mism ? 1u : 0u;
+    acc.first_tol = (mism && i < acc.first_tol) ? i : acc.first_tol;
+    acc.nf += (mism && !finite) ? 1u : 0u;
+  }
+}
+
+// Bit e set: element e of the chunk pair needs pair_slow (its bits differ,
+// or, under the strict policy, b's element is a NaN).  1- and 2-byte
+// elements are tested four or two to a word: adding 0x7F.. (0x7FFF..) to the
+// low seven (fifteen) bits sets an element's top bit iff they are non-zero,
+// and adding the gap between the largest finite magnitude and the top bit
+// does the same for a NaN; no sum carries into the next element.
+template <int DT>
+__device__ __forceinline__ uint32_t need_mask(const u32x4& va, const u32x4& vb, bool strict) {
+  constexpr int es = Et<DT>::es;
+  constexpr bool fp = Et<DT>::fp;
+  uint32_t mask = 0;
+  if constexpr (es == 8) {
+    mask |= ((va.x ^ vb.x) | (va.y ^ vb.y)) != 0u ? 1u : 0u;
+    mask |= ((va.z ^ vb.z) | (va.w ^ vb.w)) != 0u ? 2u : 0u;
+  } else if constexpr (es == 4) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      bool need = (va[k] ^ vb[k]) != 0u;
+      if constexpr (fp) need = need || (strict && (vb[k] & 0x7FFFFFFFu) > 0x7F800000u);
+      mask |= need ? (1u << k) : 0u;
     }
-    if (mism) {
-      acc.tol += 1;
-      acc.first_tol = i < acc.first_tol ? i : acc.first_tol;
-      if (nonfinite) acc.nf += 1;
+  } else if constexpr (es == 2) {
+    constexpr uint32_t kNanGap = DT == ASMEVO_F16 ? 0x03FF03FFu : 0x007F007Fu;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t x = va[k] ^ vb[k];
+      uint32_t top = ((x & 0x7FFF7FFFu) + 0x7FFF7FFFu) | x;
+      if constexpr (fp) top |= strict ? (vb[k] & 0x7FFF7FFFu) + kNanGap : 0u;
+      top &= 0x80008000u;
+      mask |= (((top >> 15) & 1u) | (top >> 30)) << (2 * k);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t x = va[k] ^ vb[k];
+      uint32_t top = ((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x;
+      if constexpr (fp) top |= strict ? (vb[k] & 0x7F7F7F7Fu) + 0x01010101u : 0u;
+      top &= 0x80808080u;
+      mask |= (((top >> 7) | (top >> 14) | (top >> 21) | (top >> 28)) & 0xFu) << (4 * k);
     }
   }
+  return mask;
 }
 
 // Logical index of walk position q of a reordered N-D segment.
@@ -153,14 +209,7 @@ __device__ __forceinline__ void chunk(const u32x4& va, const u32x4& vb, uint64_t
                                       bool permuted = false) {
   const u32x4 x = va ^ vb;
   if (((x.x | x.y | x.z | x.w) == 0u) && !strict) return;   // the common case
-  constexpr int es = Et<DT>::es;
-  constexpr int epc = 16 / es;
-  uint32_t mask = 0;
-#pragma unroll
-  for (int e = 0; e < epc; ++e) {
-    const bool need = elem<DT>(x, e) != 0 || (strict && is_nan_raw<DT>(elem<DT>(vb, e)));
-    mask |= need ? (1u << e) : 0u;
-  }
+  uint32_t mask = need_mask<DT>(va, vb, strict);
   mask &= (nvalid >= 32u) ? ~0u : ((1u << nvalid) - 1u);
   while (mask) {
     const uint32_t e = (uint32_t)__builtin_ctz(mask);
@@ -616,7 +665,11 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       u32x4 x = va[0] ^ vb[0];
 #pragma unroll
       for (int j = 1; j < U; ++j) x |= va[j] ^ vb[j];
-      if (((x.x | x.y | x.z | x.w) != 0u) || strict) {
+      // (unlikely: the slow path is then laid out away from the loop, which
+      // runs straight through to the next tile's loads with one taken branch;
+      // with the slow path inline and jumped over, the sweep measured 1-2 %
+      // slower)
+      if (__builtin_expect(((x.x | x.y | x.z | x.w) != 0u) || strict, 0)) {
 #pragma unroll
         for (int j = 0; j < U; ++j)
           chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
