@@ -29,7 +29,8 @@
  *  - `workspace` is device memory of at least asmevo_workspace_bytes(...)
  *    bytes, owned by the caller; the call stages its descriptor tables there.
  *    It must not be reused by another call until this call's work on `stream`
- *    has completed.  The library allocates no memory of its own.
+ *    has completed.  The library allocates no memory of its own, apart from
+ *    the asmevo_va_alloc calls, which exist to allocate.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
  *    asynchronously; results are defined once the stream has been
  *    synchronised.  The descriptor upload is a host-to-device copy from
@@ -383,6 +384,41 @@ typedef struct {
  */
 asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n,
                                   void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Device memory at a chosen virtual address (section 3.4, Tier 2: a captured
+ * pre-dispatch state holds absolute device pointers, so replaying it, here or
+ * in another process, needs its regions back at the addresses they were
+ * captured at).  These are the library's only allocating calls; everything
+ * else works on caller-owned memory.
+ *
+ * asmevo_va_granularity -- the size and address granularity of the calls
+ * below for the current device, in bytes; 0 if the device has no virtual
+ * memory management (HIP's hipMemAddressReserve family).
+ *
+ * asmevo_va_alloc -- reserves `bytes` of device address space starting at
+ * `addr` (0: wherever the driver chooses), backs it with memory of the
+ * current device, maps it readable and writable, and stores its address in
+ * *out.  Contents are undefined.  `addr` and `bytes` must be multiples of
+ * asmevo_va_granularity().  A range that cannot be placed at `addr` (already
+ * in use, or outside the device's address aperture) is released again and the
+ * call returns ASMEVO_E_UNSUPPORTED.  A range freed in this process can be
+ * requested again.  A state meant for replay in another process is best
+ * placed at an explicit address: the addresses the driver picks lie near the
+ * top of the device aperture, where a new process's runtime places its own
+ * allocations (on MI355X under ROCm 7 explicit addresses from 2^44 to
+ * 0x4F00'0000'0000 were honoured in fresh processes; 0x7F00'0000'0000 lies
+ * outside the aperture).  Errors: ASMEVO_E_INVALID (null out, zero or
+ * unaligned size or address), ASMEVO_E_UNSUPPORTED, ASMEVO_E_HIP.
+ * Synchronous.
+ *
+ * asmevo_va_free -- unmaps and releases a range returned by asmevo_va_alloc
+ * (its start address).  The caller makes sure no queued work still uses it.
+ * Errors: ASMEVO_E_INVALID (not a live range of this process), ASMEVO_E_HIP.
+ */
+size_t asmevo_va_granularity(void);
+asmevo_status asmevo_va_alloc(uint64_t addr, uint64_t bytes, uint64_t* out);
+asmevo_status asmevo_va_free(uint64_t addr);
 
 /* Workspace bytes sufficient for any of the three calls with up to n_descs
  * descriptors and n_inj injections. */

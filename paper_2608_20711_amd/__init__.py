@@ -124,7 +124,8 @@ EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments
             "asmevo_guard_check", "asmevo_workspace_bytes", "asmevo_status_string",
             "asmevo_abi_version", "asmevo_last_hip_error", "asmevo_diff_segments_nd",
             "asmevo_diff_nd_workspace_bytes", "asmevo_kernel_load", "asmevo_kernel_unload",
-            "asmevo_kernel_launch", "asmevo_kernel_time"]
+            "asmevo_kernel_launch", "asmevo_kernel_time", "asmevo_va_granularity", "asmevo_va_alloc",
+            "asmevo_va_free"]
 
 
 class AsmevoError(RuntimeError):
@@ -144,6 +145,10 @@ def _lib() -> ctypes.CDLL:
     if _handle is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2608_20711_amd.build)")
+        # torch first: it loads the HIP runtime its tensors and streams live
+        # in, and the library must then run on that same runtime (loaded the
+        # other way round, torch found no GPU in a fresh process)
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         vp, P = ctypes.c_void_p, ctypes.POINTER
         L.asmevo_fill_guarded.argtypes = [P(Alloc), ctypes.c_int32, P(Injection), ctypes.c_int64,
@@ -184,6 +189,12 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_status_string.restype = ctypes.c_char_p
         L.asmevo_abi_version.restype = ctypes.c_int32
         L.asmevo_last_hip_error.restype = ctypes.c_int32
+        L.asmevo_va_granularity.argtypes = []
+        L.asmevo_va_granularity.restype = ctypes.c_size_t
+        L.asmevo_va_alloc.argtypes = [ctypes.c_uint64, ctypes.c_uint64, P(ctypes.c_uint64)]
+        L.asmevo_va_alloc.restype = ctypes.c_int32
+        L.asmevo_va_free.argtypes = [ctypes.c_uint64]
+        L.asmevo_va_free.restype = ctypes.c_int32
         _handle = L
     return _handle
 
@@ -276,6 +287,22 @@ def copy_regions(regions: Sequence[Region], workspace_ptr: int, workspace_size: 
     r = _array(Region, regions)
     _check(_lib().asmevo_copy_regions(r, len(regions), workspace_ptr, workspace_size, _stream_handle(stream)),
            "asmevo_copy_regions")
+
+
+def va_granularity() -> int:
+    """Size and address granularity of va_alloc on the current device (0: unsupported)."""
+    return int(_lib().asmevo_va_granularity())
+
+
+def va_alloc(nbytes: int, addr: int = 0) -> int:
+    """Device memory mapped at `addr` (0: anywhere); returns its address."""
+    out = ctypes.c_uint64(0)
+    _check(_lib().asmevo_va_alloc(addr, nbytes, ctypes.byref(out)), "asmevo_va_alloc")
+    return int(out.value)
+
+
+def va_free(addr: int) -> None:
+    _check(_lib().asmevo_va_free(addr), "asmevo_va_free")
 
 
 def guard_check(allocs: Sequence[Alloc], seed: int, results_ptr: int, workspace_ptr: int,

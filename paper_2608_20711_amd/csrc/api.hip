@@ -12,6 +12,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <vector>
 
 #include "asmevo.h"
@@ -873,6 +874,112 @@ asmevo_status asmevo_kernel_time(const asmevo_kernel* k, const uint32_t grid[3],
   for (auto& e : ev)
     if (e) (void)hipEventDestroy(e);
   return result;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Device memory at chosen virtual addresses (Tier-2 replay of captured state).
+
+namespace {
+
+struct VaRange {
+  uint64_t bytes;
+  hipMemGenericAllocationHandle_t handle;
+};
+std::mutex g_va_mutex;
+std::map<uint64_t, VaRange> g_va;   // live ranges of this process, by start address
+
+hipMemAllocationProp va_prop(int dev) {
+  hipMemAllocationProp prop;
+  std::memset(&prop, 0, sizeof(prop));
+  prop.type = hipMemAllocationTypePinned;
+  prop.location.type = hipMemLocationTypeDevice;
+  prop.location.id = dev;
+  return prop;
+}
+
+size_t va_granularity_of(int dev) {
+  int vmm = 0;
+  if (hipDeviceGetAttribute(&vmm, hipDeviceAttributeVirtualMemoryManagementSupported, dev) != hipSuccess || !vmm)
+    return 0;
+  const hipMemAllocationProp prop = va_prop(dev);
+  size_t gran = 0;
+  if (hipMemGetAllocationGranularity(&gran, &prop, hipMemAllocationGranularityMinimum) != hipSuccess) return 0;
+  return gran;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t asmevo_va_granularity(void) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  return va_granularity_of(dev);
+}
+
+asmevo_status asmevo_va_alloc(uint64_t addr, uint64_t bytes, uint64_t* out) {
+  if (!out || bytes == 0) return ASMEVO_E_INVALID;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  const size_t gran = va_granularity_of(dev);
+  if (gran == 0) return ASMEVO_E_UNSUPPORTED;
+  if (bytes % gran != 0 || addr % gran != 0) return ASMEVO_E_INVALID;
+  const hipMemAllocationProp prop = va_prop(dev);
+  void* p = nullptr;
+  const hipError_t er = hipMemAddressReserve(&p, (size_t)bytes, gran, reinterpret_cast<void*>(addr), 0);
+  if (er != hipSuccess) {
+    g_last_hip = (int32_t)er;
+    return addr != 0 ? ASMEVO_E_UNSUPPORTED : ASMEVO_E_HIP;
+  }
+  if (addr != 0 && reinterpret_cast<uint64_t>(p) != addr) {
+    (void)hipMemAddressFree(p, (size_t)bytes);
+    return ASMEVO_E_UNSUPPORTED;
+  }
+  hipMemGenericAllocationHandle_t h;
+  hipError_t e = hipMemCreate(&h, (size_t)bytes, &prop, 0);
+  if (e != hipSuccess) {
+    (void)hipMemAddressFree(p, (size_t)bytes);
+    g_last_hip = (int32_t)e;
+    return ASMEVO_E_HIP;
+  }
+  e = hipMemMap(p, (size_t)bytes, 0, h, 0);
+  if (e == hipSuccess) {
+    hipMemAccessDesc acc;
+    std::memset(&acc, 0, sizeof(acc));
+    acc.location = prop.location;
+    acc.flags = hipMemAccessFlagsProtReadWrite;
+    e = hipMemSetAccess(p, (size_t)bytes, &acc, 1);
+    if (e != hipSuccess) (void)hipMemUnmap(p, (size_t)bytes);
+  }
+  if (e != hipSuccess) {
+    (void)hipMemRelease(h);
+    (void)hipMemAddressFree(p, (size_t)bytes);
+    g_last_hip = (int32_t)e;
+    // a requested address the driver reserved but cannot map lies outside the
+    // device's aperture
+    return addr != 0 ? ASMEVO_E_UNSUPPORTED : ASMEVO_E_HIP;
+  }
+  {
+    std::lock_guard<std::mutex> lock(g_va_mutex);
+    g_va[reinterpret_cast<uint64_t>(p)] = VaRange{bytes, h};
+  }
+  *out = reinterpret_cast<uint64_t>(p);
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_va_free(uint64_t addr) {
+  std::lock_guard<std::mutex> lock(g_va_mutex);
+  auto it = g_va.find(addr);
+  if (it == g_va.end()) return ASMEVO_E_INVALID;
+  void* p = reinterpret_cast<void*>(addr);
+  const VaRange r = it->second;
+  HIP_TRY(hipMemUnmap(p, (size_t)r.bytes));
+  g_va.erase(it);                       // unmapped: the range is no longer usable
+  HIP_TRY(hipMemRelease(r.handle));
+  HIP_TRY(hipMemAddressFree(p, (size_t)r.bytes));
+  return ASMEVO_OK;
 }
 
 }  // extern "C"

@@ -215,6 +215,19 @@ def test_copy_regions_workspace():
     assert e.value.status == lib.E_WORKSPACE
 
 
+def test_va_argument_errors():
+    L = lib.lib()
+    out = ctypes.c_uint64(0)
+    assert L.asmevo_va_alloc(0, 0, ctypes.byref(out)) == lib.E_INVALID          # zero bytes
+    assert L.asmevo_va_alloc(0, 1 << 21, None) == lib.E_INVALID                 # no output
+    assert L.asmevo_va_free(0x7000_0000_0000) == lib.E_INVALID                  # not a live range
+    assert out.value == 0
+    assert lib.va_granularity() >= 0
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.va_free(0x1000)
+    assert e.value.status == lib.E_INVALID
+
+
 def _seg_nd(shape=(4, 8), sa=(8, 1), sb=(8, 1), **kw):
     d = dict(a=0x10000, b=0x20000, dtype=lib.F32, mode=lib.TOLERANCE, nan_policy=0, shape=shape,
              stride_a=sa, stride_b=sb)

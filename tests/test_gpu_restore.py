@@ -69,3 +69,31 @@ def test_snapshot_restore_replay():
     after = st.arena_host("cand")
     for o, n in regions:
         assert_bytes_equal(after[o:o + n], before[o:o + n], f"region at {o}")
+
+
+def test_va_alloc_in_use_and_again():
+    """A range handed out by asmevo_va_alloc cannot be requested while it is
+    live, and can be requested again, at the same address, once freed."""
+    gran = lib.va_granularity()
+    assert gran > 0, "the device has no virtual memory management"
+    size = 64 * gran
+    a = lib.va_alloc(size)
+    assert a % gran == 0
+    with pytest.raises(lib.AsmevoError) as e:
+        lib.va_alloc(size, a)
+    assert e.value.status == lib.E_UNSUPPORTED
+    lib.va_free(a)
+    assert lib.va_alloc(size, a) == a
+    # the range is usable memory: a pattern copied in comes back out
+    pattern = torch.from_numpy(np.random.default_rng(5).integers(0, 256, size=size, dtype=np.uint8)).cuda()
+    back = torch.empty_like(pattern)
+    ws_size = lib.workspace_bytes(1)
+    ws = torch.empty(ws_size, dtype=torch.uint8, device="cuda")
+    lib.copy_regions([lib.Region(a, pattern.data_ptr(), size)], ws.data_ptr(), ws_size)
+    lib.copy_regions([lib.Region(back.data_ptr(), a, size)], ws.data_ptr(), ws_size)
+    torch.cuda.synchronize()
+    assert torch.equal(back, pattern)
+    lib.va_free(a)
+    with pytest.raises(lib.AsmevoError):
+        lib.va_free(a)
+
