@@ -143,6 +143,7 @@ def lib() -> ctypes.CDLL:
         L.ref_diff_segment.argtypes = [P(RefSeg), vp, vp, P(RefSegResult)]
         L.ref_diff_segment_nd.argtypes = [P(RefSegND), vp, vp, P(RefSegResult)]
         L.ref_cosine_segment.argtypes = [P(RefSeg), vp, vp, P(RefCosResult)]
+        L.ref_cosine_nd.argtypes = [P(RefSegND), ctypes.c_int32, vp, vp, P(RefCosResult)]
         L.ref_pairwise_tree.argtypes = [vp, ctypes.c_int64]
         L.ref_pairwise_tree.restype = ctypes.c_double
         L.ref_copy_regions.argtypes = [P(RefRegion), ctypes.c_int64]
@@ -352,6 +353,31 @@ def cosine_segment(dtype: str, rows: int, cols: int, stride_a: int, stride_b: in
     rc = lib().ref_cosine_segment(ctypes.byref(seg), _ptr(a) + a_off, _ptr(b) + b_off, ctypes.byref(res))
     if rc != 0:
         raise ValueError("oracle cosine rejected the segment")
+    return res.as_dict()
+
+
+def cosine_nd(dtype: str, parts: Sequence, a: np.ndarray, b: np.ndarray) -> Dict:
+    """Cosine term of one result over N-D segments in the walk order (see
+    ref_oracle.h).  parts: (shape, stride_a, stride_b, a_off, b_off) per
+    segment, in segment order; strides in elements, offsets in bytes of the
+    uint8 arrays a and b."""
+    n = len(parts)
+    segs = (RefSegND * max(n, 1))()
+    a = np.ascontiguousarray(a).view(np.uint8)
+    b = np.ascontiguousarray(b).view(np.uint8)
+    pa = (ctypes.c_void_p * max(n, 1))()
+    pb = (ctypes.c_void_p * max(n, 1))()
+    for k, (shape, sa, sb, a_off, b_off) in enumerate(parts):
+        nd = len(shape)
+        assert nd <= MAX_DIMS and len(sa) == nd and len(sb) == nd
+        segs[k] = RefSegND(DTYPE[dtype], MODE["bitwise"], 0, nd, 0, (ctypes.c_int64 * MAX_DIMS)(*shape),
+                           (ctypes.c_int64 * MAX_DIMS)(*sa), (ctypes.c_int64 * MAX_DIMS)(*sb), 0.0, 0.0)
+        pa[k] = _ptr(a) + a_off
+        pb[k] = _ptr(b) + b_off
+    res = RefCosResult()
+    rc = lib().ref_cosine_nd(segs, n, pa, pb, ctypes.byref(res))
+    if rc != 0:
+        raise ValueError("oracle N-D cosine rejected the segments")
     return res.as_dict()
 
 

@@ -771,6 +771,165 @@ int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, r
   return 0;
 }
 
+/* The walk of an N-D segment: dimensions of extent > 1, stably ordered by
+ * decreasing stride of a (a stride of 0 counts as the largest), ties by
+ * decreasing stride of b; then, from the innermost, a dimension that steps
+ * exactly over the whole of the next-inner one in both operands is merged
+ * into it.  Returns the merged dimensions, outermost first (at least one). */
+typedef struct {
+  int64_t n, sa, sb;
+} walk_dim;
+
+static int64_t stride_key(int64_t v) { return v == 0 ? INT64_MAX : v; }
+
+static int walk_of(const ref_seg_nd* seg, walk_dim* out) {
+  walk_dim d[REF_MAX_DIMS];
+  int nd = 0;
+  for (int k = 0; k < seg->ndim; ++k) {
+    if (seg->shape[k] <= 1) continue;
+    walk_dim v = {seg->shape[k], seg->stride_a[k], seg->stride_b[k]};
+    int j = nd++;
+    /* insertion: v goes before every earlier entry it orders before */
+    while (j > 0) {
+      walk_dim u = d[j - 1];
+      int before = stride_key(v.sa) != stride_key(u.sa) ? stride_key(v.sa) > stride_key(u.sa)
+                                                         : stride_key(v.sb) > stride_key(u.sb);
+      if (!before) break;
+      d[j] = u;
+      --j;
+    }
+    d[j] = v;
+  }
+  walk_dim m[REF_MAX_DIMS];
+  int nm = 0;
+  for (int k = nd - 1; k >= 0; --k) {
+    if (nm > 0 && d[k].sa == m[nm - 1].n * m[nm - 1].sa && d[k].sb == m[nm - 1].n * m[nm - 1].sb)
+      m[nm - 1].n *= d[k].n;
+    else
+      m[nm++] = d[k];
+  }
+  if (nm == 0) {
+    m[0].n = 1;
+    m[0].sa = 1;
+    m[0].sb = 1;
+    nm = 1;
+  }
+  for (int k = 0; k < nm; ++k) out[k] = m[nm - 1 - k];
+  return nm;
+}
+
+/* Block sums of one row of len elements, element t at a + t*step_a and
+ * b + t*step_b (bytes), appended at bab/baa/bbb[*k]. */
+static void row_block_sums(int32_t dtype, int es, const uint8_t* a, const uint8_t* b, int64_t step_a,
+                           int64_t step_b, int64_t len, double* bab, double* baa, double* bbb, int64_t* k,
+                           uint64_t* pairs) {
+  int64_t per_block = 4096 / es, per_chunk = 16 / es;
+  for (int64_t c0 = 0; c0 < len; c0 += per_block, ++*k) {
+    double lab[64], laa[64], lbb[64];
+    for (int L = 0; L < 64; ++L) lab[L] = laa[L] = lbb[L] = 0.0;
+    int64_t n = len - c0 < per_block ? len - c0 : per_block;
+    for (int64_t t = 0; t < n; ++t) {
+      uint64_t ra = load_raw(a + (c0 + t) * step_a, es);
+      uint64_t rb = load_raw(b + (c0 + t) * step_b, es);
+      double A, B;
+      if (ref_decode(dtype, ra, &A) != 0 || ref_decode(dtype, rb, &B) != 0) continue;
+      int L = (int)((t / per_chunk) % 64);
+      lab[L] = lab[L] + A * B;
+      laa[L] = laa[L] + A * A;
+      lbb[L] = lbb[L] + B * B;
+      *pairs += 1;
+    }
+    for (int m = 32; m >= 1; m /= 2) {
+      double nab[64], naa[64], nbb[64];
+      for (int L = 0; L < 64; ++L) {
+        nab[L] = lab[L] + lab[L ^ m];
+        naa[L] = laa[L] + laa[L ^ m];
+        nbb[L] = lbb[L] + lbb[L ^ m];
+      }
+      for (int L = 0; L < 64; ++L) {
+        lab[L] = nab[L];
+        laa[L] = naa[L];
+        lbb[L] = nbb[L];
+      }
+    }
+    bab[*k] = lab[0];
+    baa[*k] = laa[0];
+    bbb[*k] = lbb[0];
+  }
+}
+
+int ref_cosine_nd(const ref_seg_nd* segs, int32_t n, const uint8_t* const* a, const uint8_t* const* b,
+                  ref_cos_result* res) {
+  res->sum_ab = res->sum_aa = res->sum_bb = 0.0;
+  res->cosine = NAN;
+  res->pairs = 0;
+  res->blocks = 0;
+  if (n <= 0) {
+    res->cosine = 1.0;                        /* no elements: both sums of squares are 0 */
+    return 0;
+  }
+  int32_t dtype = segs[0].dtype;
+  int es = ref_esize(dtype);
+  if (es == 0) return -1;
+  for (int32_t s = 0; s < n; ++s)
+    if (segs[s].dtype != dtype || segs[s].ndim < 0 || segs[s].ndim > REF_MAX_DIMS) return -1;
+  if (!is_float(dtype)) return 0;
+  /* first pass: blocks of every row of every segment */
+  int64_t nblocks = 0;
+  for (int32_t s = 0; s < n; ++s) {
+    int empty = 0;
+    for (int d = 0; d < segs[s].ndim; ++d) empty |= segs[s].shape[d] == 0;
+    if (empty) continue;
+    walk_dim w[REF_MAX_DIMS];
+    int nw = walk_of(&segs[s], w);
+    int64_t rows = 1;
+    for (int d = 0; d + 1 < nw; ++d) rows *= w[d].n;
+    nblocks += rows * ((w[nw - 1].n + 4096 / es - 1) / (4096 / es));
+  }
+  double* bab = (double*)malloc(sizeof(double) * (size_t)(nblocks ? nblocks : 1) * 3);
+  if (!bab) return -1;
+  double* baa = bab + nblocks;
+  double* bbb = baa + nblocks;
+  int64_t k = 0;
+  for (int32_t s = 0; s < n; ++s) {
+    int empty = 0;
+    for (int d = 0; d < segs[s].ndim; ++d) empty |= segs[s].shape[d] == 0;
+    if (empty) continue;
+    walk_dim w[REF_MAX_DIMS];
+    int nw = walk_of(&segs[s], w);
+    int64_t rows = 1;
+    for (int d = 0; d + 1 < nw; ++d) rows *= w[d].n;
+    for (int64_t r = 0; r < rows; ++r) {
+      /* outer walk index of row r, last outer dimension fastest */
+      int64_t rest = r, off_a = 0, off_b = 0;
+      for (int d = nw - 2; d >= 0; --d) {
+        int64_t idx = rest % w[d].n;
+        rest /= w[d].n;
+        off_a += idx * w[d].sa;
+        off_b += idx * w[d].sb;
+      }
+      row_block_sums(dtype, es, a[s] + off_a * es, b[s] + off_b * es, w[nw - 1].sa * es, w[nw - 1].sb * es,
+                     w[nw - 1].n, bab, baa, bbb, &k, &res->pairs);
+    }
+  }
+  res->blocks = (uint64_t)nblocks;
+  res->sum_ab = ref_pairwise_tree(bab, nblocks);
+  res->sum_aa = ref_pairwise_tree(baa, nblocks);
+  res->sum_bb = ref_pairwise_tree(bbb, nblocks);
+  free(bab);
+  if (res->sum_aa == 0.0 && res->sum_bb == 0.0) {
+    res->cosine = 1.0;
+  } else if (res->sum_aa == 0.0 || res->sum_bb == 0.0) {
+    res->cosine = 0.0;
+  } else {
+    double na = sqrt(res->sum_aa);
+    double nb = sqrt(res->sum_bb);
+    double den = na * nb;
+    res->cosine = res->sum_ab / den;
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Tier-2 state restore: plain byte copies.                                  */
 /* ------------------------------------------------------------------------ */

@@ -139,6 +139,16 @@ typedef struct {
   uint64_t blocks;
 } ref_cos_result;
 int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res);
+/* The same term over n N-D segments that share one result, in the walk
+ * order: in each segment the dimensions of extent > 1 are ordered by
+ * decreasing stride of a (stride 0 first), ties by decreasing stride of b,
+ * then neighbours contiguous in both operands are merged; the innermost
+ * merged dimension forms rows, the others order them (last fastest); rows are
+ * cut into blocks as above, and the blocks of all n segments, in segment
+ * order, combine by the pairwise tree.  a[k], b[k]: element (0, ..., 0) of
+ * segment k.  Every segment must have the same float dtype. */
+int ref_cosine_nd(const ref_seg_nd* segs, int32_t n, const uint8_t* const* a, const uint8_t* const* b,
+                  ref_cos_result* res);
 /* the left-complete pairwise tree alone (exposed for its pins) */
 double ref_pairwise_tree(const double* x, int64_t n);
 

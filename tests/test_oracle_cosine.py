@@ -5,7 +5,11 @@ xor butterfly, left-complete pairwise tree over blocks).  What pins it:
 exactly representable cases (small integers) against exact integer sums;
 hand-computed cases where this association gives a different result than a
 sequential sum; the perfect pairwise tree against numpy's level-by-level
-pairing; and the error bound of the result against math.fsum."""
+pairing; and the error bound of the result against math.fsum.  The N-D
+form (segments walked in memory order, several sharing a result) is pinned by
+its reduction to the pinned 1-row and 2-D forms on contiguous and padded
+views, by exact integer sums and block counts that follow from the walk on
+transposed and broadcast views, and by the pinned tree over segments."""
 import math
 
 import numpy as np
@@ -188,3 +192,77 @@ def test_nonfinite_pairs_are_excluded():
     assert r["pairs"] == 9000 - 4
     for k in ("sum_ab", "sum_aa", "sum_bb", "cosine"):
         assert r[k] == r0[k]
+
+
+# ---------------------------------------------------------------- N-D segments
+def _bits(x):
+    import struct
+    return {k: (struct.unpack("<Q", struct.pack("<d", v))[0] if isinstance(v, float) else v) for k, v in x.items()}
+
+
+@pytest.mark.parametrize("dtype,np_t", [("f32", np.float32), ("f16", np.float16)])
+def test_nd_contiguous_views_reduce_to_one_row(dtype, np_t):
+    """A contiguous tensor of any shape (unit dimensions included) walks as one
+    row: the N-D cosine equals the 1-row cosine of the flat buffer, bit for
+    bit; a padded 2-D view equals the 2-D cosine with the same pitch."""
+    rng = np.random.default_rng(7)
+    a = rng.standard_normal(6 * 1 * 5 * 700).astype(np_t)
+    b = (a + rng.standard_normal(a.size).astype(np_t) * np_t(0.01)).astype(np_t)
+    flat = _cos(dtype, a, b)
+    nd = oracle.cosine_nd(dtype, [([6, 1, 5, 700], [3500, 3500, 700, 1], [3500, 3500, 700, 1], 0, 0)],
+                          a.view(np.uint8), b.view(np.uint8))
+    assert _bits(nd) == _bits(flat)
+    rows, cols, pitch = 30, 600, 700
+    two_d = _cos(dtype, a, b, rows, cols, pitch, pitch)
+    nd2 = oracle.cosine_nd(dtype, [([rows, cols], [pitch, 1], [pitch, 1], 0, 0)], a.view(np.uint8),
+                           b.view(np.uint8))
+    assert _bits(nd2) == _bits(two_d)
+    assert nd2["blocks"] == rows                      # 600 elements per row: one block each
+
+
+def test_nd_walk_order_blocks_and_exact_sums():
+    """Views whose walk differs from the logical order: a transposed matrix
+    walks memory order and merges into one row; a broadcast operand keeps
+    rows apart.  With small integers every sum is exact, so the sums equal the
+    integer dot products, and the block counts follow from the walk."""
+    rng = np.random.default_rng(8)
+    R, C = 96, 80                                     # a is stored [C, R]; the view is [R, C] (transposed)
+    ai = rng.integers(-8, 9, size=(C, R))
+    bi = rng.integers(-8, 9, size=(C, R))
+    a = ai.astype(np.float32)
+    b = bi.astype(np.float32)
+    t = oracle.cosine_nd("f32", [([R, C], [1, R], [1, R], 0, 0)], a.view(np.uint8), b.view(np.uint8))
+    assert t["sum_ab"] == float((ai * bi).sum()) and t["sum_aa"] == float((ai * ai).sum())
+    assert t["sum_bb"] == float((bi * bi).sum())
+    assert t["blocks"] == -(-(R * C) // 1024) and t["pairs"] == R * C
+    # b broadcast along rows: 64 rows of 128 elements, one block each
+    rows, cols = 64, 128
+    ai = rng.integers(-8, 9, size=(rows, cols))
+    bi = rng.integers(-8, 9, size=cols)
+    a = ai.astype(np.float32)
+    b = bi.astype(np.float32)
+    r = oracle.cosine_nd("f32", [([rows, cols], [cols, 1], [0, 1], 0, 0)], a.view(np.uint8), b.view(np.uint8))
+    assert r["blocks"] == rows and r["pairs"] == rows * cols
+    assert r["sum_ab"] == float((ai * bi[None, :]).sum()) and r["sum_bb"] == float(rows * (bi * bi).sum())
+
+
+def test_nd_segments_sharing_a_result_concatenate_blocks():
+    """Several segments of one result: their blocks, in segment order, form
+    one tree.  With one block per segment, the result's sums are the pairwise
+    tree of the per-segment sums (checked against the tree routine, itself
+    pinned above), and exact integer data gives exact totals."""
+    rng = np.random.default_rng(9)
+    n_seg, blk = 5, 256                               # 256 fp32 elements: one block per segment
+    a = rng.standard_normal(n_seg * blk).astype(np.float32)
+    b = rng.standard_normal(n_seg * blk).astype(np.float32)
+    parts = [([blk], [1], [1], 4 * blk * k, 4 * blk * k) for k in range(n_seg)]
+    whole = oracle.cosine_nd("f32", parts, a.view(np.uint8), b.view(np.uint8))
+    singles = [oracle.cosine_nd("f32", [p], a.view(np.uint8), b.view(np.uint8)) for p in parts]
+    assert whole["blocks"] == n_seg and whole["pairs"] == n_seg * blk
+    for f in ("sum_ab", "sum_aa", "sum_bb"):
+        assert whole[f] == oracle.pairwise_tree(np.array([s[f] for s in singles]))
+    ai = rng.integers(-8, 9, size=n_seg * blk)
+    a = ai.astype(np.float32)
+    e = oracle.cosine_nd("f32", parts[::-1], a.view(np.uint8), a.view(np.uint8))
+    assert e["sum_ab"] == float((ai * ai).sum()) and abs(e["cosine"] - 1.0) <= 2.0 ** -52
+    assert oracle.cosine_nd("f32", [], a.view(np.uint8), a.view(np.uint8))["blocks"] == 0
