@@ -153,8 +153,9 @@ def cpu_model() -> str:
 
 
 def nd_cases(st, stream, steps: int, scratch):
-    """Times asmevo_diff_segments_nd on views of the first (up to) 16 GiB of the
-    candidate and reference arenas, read as fp32 tensors."""
+    """Times asmevo_diff_segments_nd, and asmevo_diff_cosine_nd, on views of the
+    first (up to) 16 GiB of the candidate and reference arenas, read as fp32
+    tensors."""
     import numpy as np
     import torch
 
@@ -209,6 +210,22 @@ def nd_cases(st, stream, steps: int, scratch):
                      "logical_bytes_per_side": 4 * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
                      "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2)}
         del ws
+        # the same view with the cosine term (asmevo_diff_cosine_nd: row-tiled walk, block trees)
+        cws = torch.empty(lib.diff_cosine_nd_workspace_bytes(segs, 1), dtype=torch.uint8, device=st.cand.device)
+        cres = torch.empty(64, dtype=torch.uint8, device=st.cand.device)
+        times = []
+        for _ in range(steps + 1):
+            if scratch is not None:
+                scratch.fill_(0x78)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            lib.diff_cosine_nd(segs, res.data_ptr(), 1, cres.data_ptr(), cws.data_ptr(), cws.numel(), stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        med = statistics.median(times[1:])
+        out[name]["cosine"] = {"ms_median": round(med, 4), "GBps": round(2 * 4 * elems / (med * 1e-3) / 1e9, 2)}
+        del cws
     return out
 
 

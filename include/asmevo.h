@@ -285,7 +285,7 @@ size_t asmevo_diff_nd_workspace_bytes(int32_t n);
  * every segment accumulates into results[segs[k].result].  The planner drops
  * unit dimensions and merges dimensions that are contiguous in both
  * operands, so a contiguous tensor of any shape is one row and runs at the
- * speed of the 1-D path.  The cosine term is not computed for N-D segments.
+ * speed of the 1-D path.  asmevo_diff_cosine_nd adds the cosine term.
  * Errors: ASMEVO_E_INVALID (also: result >= n_results, ndim out of range,
  * negative shape, stride or index_base, an element offset beyond 2^52
  * bytes), ASMEVO_E_WORKSPACE.
@@ -337,6 +337,31 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
 /* Workspace bytes asmevo_diff_cosine needs for these segments (0 if they are
  * invalid). */
 size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n);
+
+/*
+ * asmevo_diff_cosine_nd -- asmevo_diff_segments_nd plus the cosine term of
+ * every result, from the same single pass.  The order of the additions is
+ * that of asmevo_diff_cosine, along each segment's walk: the dimensions of
+ * extent > 1 ordered by decreasing stride of a (stride 0 first), ties by
+ * decreasing stride of b, then neighbours contiguous in both operands merged;
+ * the innermost merged dimension forms the rows (cut into 4096-byte blocks),
+ * the other dimensions order the rows, last fastest; the blocks of all the
+ * segments of a result, in array order, combine by one pairwise tree.  (A
+ * 2-D segment of asmevo_diff_cosine walks the same way.)  The segments of a
+ * result must be consecutive in `segs` and of one element type, else
+ * ASMEVO_E_UNSUPPORTED; a result with no segments has cosine 1.0 over no
+ * blocks.  cos_results[0..n_results) device memory; the workspace must hold
+ * asmevo_diff_cosine_nd_workspace_bytes(segs, n, n_results) bytes.  Other
+ * errors as for asmevo_diff_segments_nd.
+ */
+asmevo_status asmevo_diff_cosine_nd(const asmevo_segment_nd* segs, int32_t n,
+                                    asmevo_segment_result* results, int32_t n_results,
+                                    asmevo_cosine_result* cos_results,
+                                    void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes asmevo_diff_cosine_nd needs (0 if the segments are invalid
+ * or unsupported, or n_results <= 0). */
+size_t asmevo_diff_cosine_nd_workspace_bytes(const asmevo_segment_nd* segs, int32_t n, int32_t n_results);
 
 /* Per-allocation guard result (48 bytes): counts of corrupted bytes and the
  * lowest corrupted byte offset within each guard (-1 if intact), and the same

@@ -125,7 +125,7 @@ EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments
             "asmevo_abi_version", "asmevo_last_hip_error", "asmevo_diff_segments_nd",
             "asmevo_diff_nd_workspace_bytes", "asmevo_kernel_load", "asmevo_kernel_unload",
             "asmevo_kernel_launch", "asmevo_kernel_time", "asmevo_va_granularity", "asmevo_va_alloc",
-            "asmevo_va_free"]
+            "asmevo_va_free", "asmevo_diff_cosine_nd", "asmevo_diff_cosine_nd_workspace_bytes"]
 
 
 class AsmevoError(RuntimeError):
@@ -189,6 +189,11 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_status_string.restype = ctypes.c_char_p
         L.asmevo_abi_version.restype = ctypes.c_int32
         L.asmevo_last_hip_error.restype = ctypes.c_int32
+        L.asmevo_diff_cosine_nd.argtypes = [P(SegmentND), ctypes.c_int32, vp, ctypes.c_int32, vp, vp,
+                                            ctypes.c_size_t, vp]
+        L.asmevo_diff_cosine_nd.restype = ctypes.c_int32
+        L.asmevo_diff_cosine_nd_workspace_bytes.argtypes = [P(SegmentND), ctypes.c_int32, ctypes.c_int32]
+        L.asmevo_diff_cosine_nd_workspace_bytes.restype = ctypes.c_size_t
         L.asmevo_va_granularity.argtypes = []
         L.asmevo_va_granularity.restype = ctypes.c_size_t
         L.asmevo_va_alloc.argtypes = [ctypes.c_uint64, ctypes.c_uint64, P(ctypes.c_uint64)]
@@ -287,6 +292,18 @@ def copy_regions(regions: Sequence[Region], workspace_ptr: int, workspace_size: 
     r = _array(Region, regions)
     _check(_lib().asmevo_copy_regions(r, len(regions), workspace_ptr, workspace_size, _stream_handle(stream)),
            "asmevo_copy_regions")
+
+
+def diff_cosine_nd_workspace_bytes(segments: Sequence[SegmentND], n_results: int) -> int:
+    s = _array(SegmentND, segments)
+    return int(_lib().asmevo_diff_cosine_nd_workspace_bytes(s, len(segments), n_results))
+
+
+def diff_cosine_nd(segments: Sequence[SegmentND], results_ptr: int, n_results: int, cos_results_ptr: int,
+                   workspace_ptr: int, workspace_size: int, stream=None) -> None:
+    s = _array(SegmentND, segments)
+    _check(_lib().asmevo_diff_cosine_nd(s, len(segments), results_ptr, n_results, cos_results_ptr, workspace_ptr,
+                                        workspace_size, _stream_handle(stream)), "asmevo_diff_cosine_nd")
 
 
 def va_granularity() -> int:

@@ -358,7 +358,8 @@ asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled,
 // and the others place them.  When the order differs from the logical one
 // the kernel maps walk positions back to logical indices on a mismatch.
 asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_results,
-                           std::vector<DiffSeg>& dev, std::vector<NdExt>& ext, uint64_t& tiles) {
+                           std::vector<DiffSeg>& dev, std::vector<NdExt>& ext, uint64_t& tiles,
+                           bool row_tiled = false) {
   if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
   dev.assign((size_t)n, DiffSeg{});
   ext.clear();
@@ -477,7 +478,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
     D.full_chunks = D.row_bytes / kChunk;
     const bool aligned = unit && S.a % 16 == 0 && S.b % 16 == 0 && pitches16;
-    const bool narrow = D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
+    const bool narrow = !row_tiled && D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
     // gathers of every other element: rows that start 16-byte aligned load whole 32-byte windows
     bool pitches16a = true, pitches16b = true;
     for (int d = 0; d + 1 < nm; ++d) {
@@ -550,6 +551,60 @@ CosPlan cos_plan(const std::vector<DiffSeg>& dev, uint64_t tiles) {
   P.off_prefix = P.off_lv + align256(n * sizeof(CosLevels));
   P.bytes = P.off_prefix + P.prefix.size() * sizeof(uint64_t);
   return P;
+}
+
+// The cosine's tree units of an N-D pass: one per result, spanning the tiles
+// of the result's segments, which must be consecutive in the array (so their
+// tiles are) and of one element type.  A result without segments is an empty
+// float unit (cosine 1.0 over no blocks).
+asmevo_status cos_units(const std::vector<DiffSeg>& dev, int32_t n_results, std::vector<DiffSeg>& units) {
+  units.assign((size_t)n_results, DiffSeg{});
+  std::vector<int64_t> last((size_t)n_results, -1);
+  for (int32_t r = 0; r < n_results; ++r) {
+    std::memset(&units[r], 0, sizeof(DiffSeg));
+    units[r].dtype = ASMEVO_F32;
+    units[r].result_index = (uint32_t)r;
+    units[r].rows = 1;
+  }
+  for (size_t k = 0; k < dev.size(); ++k) {
+    const DiffSeg& D = dev[k];
+    DiffSeg& U = units[D.result_index];
+    if (last[D.result_index] < 0) {
+      U.dtype = D.dtype;
+      U.tile_begin = D.tile_begin;
+    } else if (last[D.result_index] != (int64_t)k - 1 || U.dtype != D.dtype) {
+      return ASMEVO_E_UNSUPPORTED;
+    }
+    U.tile_count += D.tile_count;
+    U.cols += D.rows * D.cols;
+    last[D.result_index] = (int64_t)k;
+  }
+  return ASMEVO_OK;
+}
+
+// Workspace of the N-D cosine pass: the cosine tables of the units (as for
+// the 2-D pass, units in place of segments), then the segment descriptors and
+// their extensions.
+struct CosNdPlan {
+  std::vector<DiffSeg> dev, units;
+  std::vector<NdExt> ext;
+  uint64_t tiles = 0;
+  CosPlan cos;
+  size_t off_segs = 0, off_ext = 0, bytes = 0;
+};
+
+asmevo_status cos_nd_plan(const asmevo_segment_nd* segs, int32_t n, int32_t n_results, CosNdPlan& P) {
+  asmevo_status st = plan_diff_nd(segs, n, n_results, P.dev, P.ext, P.tiles, true);
+  if (st != ASMEVO_OK) return st;
+  st = cos_units(P.dev, n_results, P.units);
+  if (st != ASMEVO_OK) return st;
+  P.cos = cos_plan(P.units, P.tiles);
+  for (const CosLevels& L : P.cos.lv)
+    if (L.cnt[kCosLevels - 1] > 255) return ASMEVO_E_UNSUPPORTED;
+  P.off_segs = align256(P.cos.bytes);
+  P.off_ext = P.off_segs + align256(P.dev.size() * sizeof(DiffSeg));
+  P.bytes = P.off_ext + P.ext.size() * sizeof(NdExt);
+  return ASMEVO_OK;
 }
 
 }  // namespace
@@ -650,6 +705,49 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
                       reinterpret_cast<const CosLevels*>(ws + P.off_lv),
                       reinterpret_cast<const uint64_t*>(ws + P.off_prefix), P.groups,
                       reinterpret_cast<double*>(ws + P.off_levels)));
+  return ASMEVO_OK;
+}
+
+size_t asmevo_diff_cosine_nd_workspace_bytes(const asmevo_segment_nd* segs, int32_t n, int32_t n_results) {
+  if (n < 0 || n_results <= 0 || (n > 0 && !segs)) return 0;
+  CosNdPlan P;
+  if (cos_nd_plan(segs, n, n_results, P) != ASMEVO_OK) return 0;
+  return P.bytes;
+}
+
+asmevo_status asmevo_diff_cosine_nd(const asmevo_segment_nd* segs, int32_t n, asmevo_segment_result* results,
+                                    int32_t n_results, asmevo_cosine_result* cos_results, void* workspace,
+                                    size_t ws_bytes, void* stream) {
+  if (n < 0 || n_results < 0 || (n > 0 && !segs) || (n_results > 0 && (!results || !cos_results)))
+    return ASMEVO_E_INVALID;
+  CosNdPlan P;
+  asmevo_status st = cos_nd_plan(segs, n, n_results, P);
+  if (st != ASMEVO_OK) return st;
+  if (n_results == 0) return ASMEVO_OK;
+  if (!workspace || ws_bytes < P.bytes) return ASMEVO_E_WORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  const CosPlan& C = P.cos;
+  HIP_TRY(hipMemcpyAsync(ws, P.units.data(), P.units.size() * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
+  std::vector<uint8_t> tables(C.bytes - C.off_lv, 0);   // CosLevels | prefix counts
+  std::memcpy(tables.data(), C.lv.data(), C.lv.size() * sizeof(CosLevels));
+  std::memcpy(tables.data() + (C.off_prefix - C.off_lv), C.prefix.data(), C.prefix.size() * sizeof(uint64_t));
+  HIP_TRY(hipMemcpyAsync(ws + C.off_lv, tables.data(), tables.size(), hipMemcpyHostToDevice, s));
+  if (n > 0) {
+    std::vector<uint8_t> host(P.bytes - P.off_segs, 0);  // descriptors | extensions
+    put(host, 0, P.dev);
+    put(host, P.off_ext - P.off_segs, P.ext);
+    HIP_TRY(hipMemcpyAsync(ws + P.off_segs, host.data(), host.size(), hipMemcpyHostToDevice, s));
+  }
+  const int wg = device_cus() * cos_nd_blocks_per_cu();   // the resident set
+  HIP_TRY(launch_diff_cosine_nd(reinterpret_cast<const DiffSeg*>(ws + P.off_segs),
+                                reinterpret_cast<const NdExt*>(ws + P.off_ext), n,
+                                reinterpret_cast<const DiffSeg*>(ws), n_results, P.tiles, results, wg, s,
+                                reinterpret_cast<double*>(ws + C.off_partials),
+                                reinterpret_cast<unsigned long long*>(ws + C.off_counters), cos_results,
+                                reinterpret_cast<const CosLevels*>(ws + C.off_lv),
+                                reinterpret_cast<const uint64_t*>(ws + C.off_prefix), C.groups,
+                                reinterpret_cast<double*>(ws + C.off_levels)));
   return ASMEVO_OK;
 }
 

@@ -1072,6 +1072,8 @@ int cos_blocks_per_cu() { return resident_blocks<true, false>(); }
 
 int diff_nd_blocks_per_cu() { return resident_blocks<false, true>(); }
 
+int cos_nd_blocks_per_cu() { return resident_blocks<true, true>(); }
+
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
                        double* partials, unsigned long long* nonfinite_pairs,
@@ -1126,6 +1128,40 @@ hipError_t launch_diff_nd(const DiffSeg* segs, const NdExt* ext, int n, int n_re
   const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
   hipLaunchKernelGGL((diff_kernel<false, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
                      total_tiles, results, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, const DiffSeg* units,
+                                 int n_results, uint64_t total_tiles, asmevo_segment_result* results,
+                                 int workgroups, hipStream_t stream, double* partials,
+                                 unsigned long long* nonfinite_pairs, asmevo_cosine_result* cos_results,
+                                 const CosLevels* levels_of, const uint64_t* level_prefix,
+                                 const uint64_t* level_groups, double* levels) {
+  if (n_results == 0) return hipSuccess;
+  hipLaunchKernelGGL(diff_init_kernel, dim3((n_results + 255) / 256), dim3(256), 0, stream, results, n_results,
+                     nonfinite_pairs);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (n > 0 && total_tiles > 0) {
+    const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
+    const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
+    hipLaunchKernelGGL((diff_kernel<true, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
+                       total_tiles, results, partials, nonfinite_pairs);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // the block trees run per result (a "unit": the result's segments, whose
+  // tiles are consecutive), as the 2-D pass runs them per segment
+  for (int k = 1; k < kCosLevels; ++k) {
+    if (level_groups[k] == 0) break;
+    const uint64_t grid = level_groups[k] < 65536 ? level_groups[k] : 65536;
+    hipLaunchKernelGGL(cos_level_kernel, dim3((unsigned)grid), dim3(kCosBlock), 0, stream, levels_of,
+                       level_prefix + (size_t)(k - 1) * (n_results + 1), n_results, k, partials, levels);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(cosine_kernel, dim3(n_results), dim3(kCosBlock), 0, stream, units, levels_of, partials,
+                     levels, nonfinite_pairs, cos_results);
   return hipGetLastError();
 }
 

@@ -215,6 +215,25 @@ def test_copy_regions_workspace():
     assert e.value.status == lib.E_WORKSPACE
 
 
+def test_diff_cosine_nd_argument_errors():
+    """Segments of one result must be consecutive and of one element type;
+    both are checked before anything is enqueued."""
+    def seg(result, dtype=lib.F32, a=0x10000):
+        return _seg_nd(a=a, b=a + 0x100000, dtype=dtype, result=result)
+    L = lib.lib()
+    for segs, n_res, status in (
+            ([seg(0), seg(1), seg(0)], 2, lib.E_UNSUPPORTED),                 # result 0 not consecutive
+            ([seg(0), seg(0, dtype=lib.F16)], 1, lib.E_UNSUPPORTED),          # two element types
+            ([seg(1)], 1, lib.E_INVALID),                                      # result slot out of range
+            ([seg(0)], -1, lib.E_INVALID)):
+        arr = lib.descriptor_array(segs)
+        assert lib.diff_cosine_nd_workspace_bytes(arr, n_res) == 0
+        assert L.asmevo_diff_cosine_nd(arr, len(segs), 0x1000, n_res, 0x2000, 0x3000, 1 << 30, None) == status
+    arr = lib.descriptor_array([seg(0), seg(0), seg(1)])
+    assert lib.diff_cosine_nd_workspace_bytes(arr, 2) > 0
+    assert L.asmevo_diff_cosine_nd(arr, 3, 0x1000, 2, 0x2000, 0x3000, 8, None) == lib.E_WORKSPACE
+
+
 def test_va_argument_errors():
     L = lib.lib()
     out = ctypes.c_uint64(0)
