@@ -652,15 +652,38 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     const uint64_t ibase = ibase0 + r * S.cols;
     const uint64_t k0 = kt * (uint64_t)kTileChunks;
     Cos cs{0.0, 0.0, 0.0};
-    if (vec && k0 + kTileChunks <= S.full_chunks) {
+    const bool whole = vec && k0 + kTileChunks <= S.full_chunks;
+    // The cosine variant also takes the last tile of an aligned unit-stride
+    // row here, with bounded loads: the bytes past the row's end load as zeros
+    // on both sides, and adding a +0.0 product leaves a lane sum unchanged (a
+    // lane sum starts at +0.0, so it is never -0.0).
+    if (whole || (kCos && vec && !gather)) {
       // Whole tile: issue all loads first, then one combined check.
-      const uint8_t* qa = pa + (k0 + lane) * kChunk;
-      const uint8_t* qb = pb + (k0 + lane) * kChunk;
       u32x4 va[U], vb[U];
+      uint32_t nv[U];                      // valid elements per chunk
+      if (kCos && !whole) {
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
-        va[j] = ld_nt(qa + j * kWave * kChunk);
-        vb[j] = ld_nt(qb + j * kWave * kChunk);
+        for (int j = 0; j < U; ++j) {
+          const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+          va[j] = u32x4{0u, 0u, 0u, 0u};
+          vb[j] = u32x4{0u, 0u, 0u, 0u};
+          nv[j] = 0;
+          if (c < S.row_chunks) {
+            const uint64_t rem = S.row_bytes - c * kChunk;
+            const uint32_t nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+            load_chunk<DT>(pa + c * kChunk, pb + c * kChunk, nb, true, va[j], vb[j]);
+            nv[j] = nb / es;
+          }
+        }
+      } else {
+        const uint8_t* qa = pa + (k0 + lane) * kChunk;
+        const uint8_t* qb = pb + (k0 + lane) * kChunk;
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          va[j] = ld_nt(qa + j * kWave * kChunk);
+          vb[j] = ld_nt(qb + j * kWave * kChunk);
+          nv[j] = epc;
+        }
       }
       u32x4 x = va[0] ^ vb[0];
 #pragma unroll
@@ -672,7 +695,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       if (__builtin_expect(((x.x | x.y | x.z | x.w) != 0u) || strict, 0)) {
 #pragma unroll
         for (int j = 0; j < U; ++j)
-          chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, epc, tol_mode,
+          chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, nv[j], tol_mode,
                         strict, S.atol, S.rtol, acc, X, permuted);
       }
       if constexpr (kCos) {
@@ -682,7 +705,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           cs = Cos{0.0, 0.0, 0.0};                 // this lane met a NaN or Inf: redo with checks
           // (unrolled: a run-time index would move va and vb out of registers)
 #pragma unroll
-          for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], epc, cs, nonfinite);
+          for (int j = 0; j < U; ++j) cos_chunk<DT>(va[j], vb[j], nv[j], cs, nonfinite);
         }
         cos_store(cs, partials + kCosRec * (S.tile_begin + tile), lane);
       }
