@@ -546,6 +546,71 @@ __device__ __forceinline__ void cos_store(Cos& c, double* out, uint32_t lane) {
 // All tiles [t_begin, t_end) of one segment.  COS: also the block sums of
 // each tile into `partials` (three doubles per global tile index).  ND: rows
 // are placed by the segment's N-D extension X (the 2-D code otherwise).
+// The cosine variant on rows of at most kNarrowCosChunks chunks, each one
+// block (one tile).  Tiling row by row would leave most of a wave idle: a row
+// of R chunks fills lanes 0..R-1 only.  Instead a wave-load holds G = 64 / P
+// rows, P the power of two at or above R, row g in lanes gP..gP+P-1, and the
+// block sums come from an xor butterfly over each group of P lanes.  That is
+// the block sum of the definition: in the 64-lane butterfly of a row's block,
+// the steps m >= P add lanes that hold +0.0 to lanes 0..P-1 (a lane sum is
+// never -0.0), so lane 0 ends with the butterfly over lanes 0..P-1.
+constexpr uint32_t kNarrowCosChunks = 32;
+
+template <int DT, bool ND>
+__device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
+                                                   uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
+                                                   double* partials, uint32_t& nonfinite, bool tol_mode,
+                                                   bool strict, bool vec, bool gather, bool pair2a, bool pair2b,
+                                                   uint64_t in_sa, uint64_t in_sb, uint64_t ibase0, bool permuted) {
+  constexpr int es = Et<DT>::es;
+  constexpr int epc = 16 / es;
+  const uint32_t R = (uint32_t)S.row_chunks;
+  uint32_t lg = 0;
+  while ((1u << lg) < R) ++lg;
+  const uint32_t P = 1u << lg, G = (uint32_t)kWave >> lg;
+  const uint32_t g = lane >> lg, t = lane & (P - 1);
+  const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
+  const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
+  // one chunk pair per lane in flight (registers are short in this variant)
+  for (uint64_t tile = t_begin; tile < t_end; tile += (uint64_t)step * G) {
+    const uint64_t row = tile + (uint64_t)g * step;
+    u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
+    uint32_t nb = 0;
+    if (row < t_end && t < R) {
+      const uint64_t cb = (uint64_t)t * kChunk;
+      const uint64_t rem = S.row_bytes - cb;
+      nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+      if constexpr (ND) {
+        uint64_t oa = 0, ob = 0;
+        nd_row_offsets(X, row, oa, ob);
+        load_nd_chunk<DT>(a0 + oa, b0 + ob, t, nb, vec, gather, in_sa, in_sb, pair2a, pair2b, t + 1 == R, va, vb);
+      } else {
+        load_chunk<DT>(a0 + row * S.a_pitch + cb, b0 + row * S.b_pitch + cb, nb, vec, va, vb);
+      }
+    }
+    chunk<DT, ND>(va, vb, ibase0 + row * S.cols + (uint64_t)t * epc, nb / es, tol_mode, strict, S.atol, S.rtol,
+                  acc, X, permuted);
+    Cos cs{0.0, 0.0, 0.0};
+    cos_chunk_fast<DT>(va, vb, cs);
+    if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
+      cs = Cos{0.0, 0.0, 0.0};
+      cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
+    }
+    for (uint32_t m = P >> 1; m >= 1; m >>= 1) {
+      cs.ab = cs.ab + __shfl_xor(cs.ab, (int)m, kWave);
+      cs.aa = cs.aa + __shfl_xor(cs.aa, (int)m, kWave);
+      cs.bb = cs.bb + __shfl_xor(cs.bb, (int)m, kWave);
+    }
+    if (t == 0 && row < t_end) {
+      double* rec = partials + kCosRec * (S.tile_begin + row);
+      rec[0] = cs.ab;
+      rec[1] = cs.aa;
+      rec[2] = cs.bb;
+      rec[3] = 0.0;
+    }
+  }
+}
+
 template <int DT, bool COS, bool ND>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                            uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
@@ -624,6 +689,14 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         chunk<DT, ND>(va[j], vb[j], i0[j], nb[j] / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
     }
     return;
+  }
+
+  if constexpr (kCos) {
+    if (S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks) {
+      diff_range_narrow_cos<DT, ND>(S, X, t_begin, t_end, step, lane, acc, partials, nonfinite, tol_mode, strict,
+                                    vec, gather, pair2a, pair2b, in_sa, in_sb, ibase0, permuted);
+      return;
+    }
   }
 
   // Row-tiled: every tile lies inside one row (and is one cosine block).

@@ -176,3 +176,42 @@ def test_cosine_many_small_segments_mixed_dtypes():
     want = [oracle.cosine_segment(s["dtype"], s["rows"], s["cols"], s["sa"], s["sb"], a_h, b_h, s["a_off"],
                                   s["b_off"]) for s in specs]
     assert_results_equal(got, want, "many small segments cosine")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "fp8e4m3"])
+def test_cosine_every_short_row_width(dtype):
+    """Rows of 1 to 32 chunks (plus a partial chunk, and aligned or misaligned
+    pitches) pack 64 / P rows per wave-load, P the power of two at or above
+    the row's chunks, with a butterfly over each group of P lanes: the cosine
+    of every such width, with NaN and Inf among the values, against the
+    oracle's 64-lane definition."""
+    rng = np.random.default_rng(31)
+    es = ESIZE[dtype]
+    n = (4 << 20) // es
+    vals = (rng.standard_normal(2 * n) * 2).astype(np.float32)
+    if dtype == "f32":
+        raw = vals.view(np.uint32).astype(np.uint64)
+    elif dtype == "bf16":
+        raw = (vals.view(np.uint32) >> 16).astype(np.uint64)
+    else:
+        raw = rng.integers(0, 0x7F, size=2 * n).astype(np.uint64)
+    k = rng.integers(0, 2 * n, size=2 * n // 500)
+    raw[k] = rng.integers(0, 1 << (8 * es), size=k.size, dtype=np.uint64)     # NaN / Inf among them
+    npt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[es]
+    a_h = raw[:n].astype(npt).view(np.uint8).copy()
+    b_h = raw[n:].astype(npt).view(np.uint8).copy()
+    a_d, b_d = torch.from_numpy(a_h).cuda(), torch.from_numpy(b_h).cuda()
+    epc = 16 // es
+    specs = []
+    for chunks in range(1, 33):
+        for extra, pad in ((0, 0), (epc // 2, 3), (0, epc)):
+            cols = max(1, (chunks - (1 if extra else 0)) * epc + extra)
+            pitch = cols + pad
+            rows = 37
+            if rows * pitch > n:
+                continue
+            specs.append(dict(dtype=dtype, rows=rows, cols=cols, sa=pitch, sb=pitch, a_off=0, b_off=0))
+    got = _cos_gpu(specs, a_d, b_d)
+    want = [oracle.cosine_segment(dtype, s["rows"], s["cols"], s["sa"], s["sb"], a_h, b_h, 0, 0) for s in specs]
+    assert_results_equal(got, want, f"{dtype} short rows cosine")
+    assert all(w["blocks"] == 37 for w, s in zip(want, specs) if s["sa"] > s["cols"])   # padded: a block per row
