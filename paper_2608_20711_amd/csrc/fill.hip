@@ -264,8 +264,8 @@ __device__ __forceinline__ void put_elem(uint32_t w[4], uint32_t m, uint64_t v) 
 // generator blocks: each VALUE and SELECT block is drawn once for its four
 // elements.
 template <int DT>
-__device__ __forceinline__ void data_chunk(const FillAlloc& A, const FillRule* rules, uint64_t i0,
-                                           uint64_t seed, uint32_t w[4]) {
+__device__ __forceinline__ void data_chunk(const FillAlloc& A, const FillAlloc* Ap, const FillRule* rules,
+                                           uint64_t i0, uint64_t seed, uint32_t w[4]) {
   constexpr int es = Elem<DT>::es;
   constexpr int epc = 16 / es;
   w[0] = w[1] = w[2] = w[3] = 0;
@@ -274,17 +274,24 @@ __device__ __forceinline__ void data_chunk(const FillAlloc& A, const FillRule* r
 #pragma unroll 1
     for (uint32_t blk = 0; blk < (uint32_t)(epc / 4); ++blk) {
       const uint64_t j = (i0 >> 2) + blk;
-      const U4 X = stream(seed, A.alloc_id, kValue, 0, 0, j);
+      // The value parameters are loaded again for every block (the empty asm
+      // hides that the pointer is loop-invariant): held across the loop they
+      // would be spilled and read back by v_readlane inside it.
+      const FillAlloc* q = Ap;
+      asm volatile("" : "+s"(q));
+      const U4 X = stream(seed, q->alloc_id, kValue, 0, 0, j);
       uint64_t base[4];
       if (A.dist == ASMEVO_DIST_NORMAL) {
+        const double p0 = q->p0, p1 = q->p1;
+        const bool sat = q->saturate != 0;
 #pragma unroll 1
         for (uint32_t h = 0; h < 2; ++h) {
           double z0, z1;
           box_muller(h ? X.z : X.x, h ? X.w : X.y, z0, z1);
-          const double v0 = A.p0 + A.p1 * z0;
-          const double v1 = A.p0 + A.p1 * z1;
-          const uint64_t e0 = encode_f32(DT, (float)v0, A.saturate != 0);
-          const uint64_t e1 = encode_f32(DT, (float)v1, A.saturate != 0);
+          const double v0 = p0 + p1 * z0;
+          const double v1 = p0 + p1 * z1;
+          const uint64_t e0 = encode_f32(DT, (float)v0, sat);
+          const uint64_t e1 = encode_f32(DT, (float)v1, sat);
           base[0] = h ? base[0] : e0;
           base[1] = h ? base[1] : e1;
           base[2] = h ? e0 : base[2];
@@ -365,7 +372,7 @@ __device__ __forceinline__ void general_chunk(const FillAlloc& A, const FillRule
 }
 
 template <int DT>
-__device__ __forceinline__ bool try_data_chunk(const FillAlloc& A, const FillRule* rules,
+__device__ __forceinline__ bool try_data_chunk(const FillAlloc& A, const FillAlloc* Ap, const FillRule* rules,
                                                uint64_t o, uint64_t seed, uint32_t w[4]) {
   constexpr int es = Elem<DT>::es;
   constexpr int epc = 16 / es;
@@ -377,12 +384,12 @@ __device__ __forceinline__ bool try_data_chunk(const FillAlloc& A, const FillRul
     c0 = e0 - r * A.stride;
   }
   if (c0 + epc > A.cols) return false;
-  data_chunk<DT>(A, rules, r * A.cols + c0, seed, w);
+  data_chunk<DT>(A, Ap, rules, r * A.cols + c0, seed, w);
   return true;
 }
 
-__device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillRule* rules, uint64_t o,
-                               uint64_t seed) {
+__device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillAlloc* Ap, const FillRule* rules,
+                                               uint64_t o, uint64_t seed) {
   const uint64_t glo = A.guard_lo, D = A.data_bytes, tot = A.total_bytes;
   uint32_t w[4];
   bool done = false;
@@ -396,13 +403,13 @@ __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillRul
     done = true;
   } else if (o >= glo && o + 16 <= glo + D) {
     switch (A.dtype) {
-      case ASMEVO_F32: done = try_data_chunk<ASMEVO_F32>(A, rules, o, seed, w); break;
-      case ASMEVO_BF16: done = try_data_chunk<ASMEVO_BF16>(A, rules, o, seed, w); break;
-      case ASMEVO_F16: done = try_data_chunk<ASMEVO_F16>(A, rules, o, seed, w); break;
-      case ASMEVO_FP8_E4M3: done = try_data_chunk<ASMEVO_FP8_E4M3>(A, rules, o, seed, w); break;
-      case ASMEVO_I32: done = try_data_chunk<ASMEVO_I32>(A, rules, o, seed, w); break;
-      case ASMEVO_I64: done = try_data_chunk<ASMEVO_I64>(A, rules, o, seed, w); break;
-      default: done = try_data_chunk<ASMEVO_U8>(A, rules, o, seed, w); break;
+      case ASMEVO_F32: done = try_data_chunk<ASMEVO_F32>(A, Ap, rules, o, seed, w); break;
+      case ASMEVO_BF16: done = try_data_chunk<ASMEVO_BF16>(A, Ap, rules, o, seed, w); break;
+      case ASMEVO_F16: done = try_data_chunk<ASMEVO_F16>(A, Ap, rules, o, seed, w); break;
+      case ASMEVO_FP8_E4M3: done = try_data_chunk<ASMEVO_FP8_E4M3>(A, Ap, rules, o, seed, w); break;
+      case ASMEVO_I32: done = try_data_chunk<ASMEVO_I32>(A, Ap, rules, o, seed, w); break;
+      case ASMEVO_I64: done = try_data_chunk<ASMEVO_I64>(A, Ap, rules, o, seed, w); break;
+      default: done = try_data_chunk<ASMEVO_U8>(A, Ap, rules, o, seed, w); break;
     }
   }
   if (!done) general_chunk(A, rules, o, seed, w);
@@ -440,7 +447,7 @@ __global__ __launch_bounds__(kFillBlock) void fill_kernel(const FillAlloc* __res
     while (k + 1 < n && allocs[k + 1].tile_begin <= t) ++k;
     const FillAlloc A = allocs[k];
     const uint64_t o = ((t - A.tile_begin) * kWave + lane) * kChunk;
-    if (o < A.total_bytes) fill_one_chunk(A, rules, o, seed);
+    if (o < A.total_bytes) fill_one_chunk(A, allocs + k, rules, o, seed);
   }
 }
 
