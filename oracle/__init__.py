@@ -93,7 +93,7 @@ class RefSegResult(ctypes.Structure):
 
 class RefCosResult(ctypes.Structure):
     _fields_ = [("sum_ab", ctypes.c_double), ("sum_aa", ctypes.c_double), ("sum_bb", ctypes.c_double),
-                ("cosine", ctypes.c_double), ("pairs", ctypes.c_uint64), ("blocks", ctypes.c_uint64)]
+                ("cosine", ctypes.c_double), ("pairs", ctypes.c_uint64), ("sum_abs_ab", ctypes.c_double)]
 
     def as_dict(self) -> Dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -144,8 +144,8 @@ def lib() -> ctypes.CDLL:
         L.ref_diff_segment_nd.argtypes = [P(RefSegND), vp, vp, P(RefSegResult)]
         L.ref_cosine_segment.argtypes = [P(RefSeg), vp, vp, P(RefCosResult)]
         L.ref_cosine_nd.argtypes = [P(RefSegND), ctypes.c_int32, vp, vp, P(RefCosResult)]
-        L.ref_pairwise_tree.argtypes = [vp, ctypes.c_int64]
-        L.ref_pairwise_tree.restype = ctypes.c_double
+        L.ref_exact_sum.argtypes = [vp, ctypes.c_int64]
+        L.ref_exact_sum.restype = ctypes.c_double
         L.ref_copy_regions.argtypes = [P(RefRegion), ctypes.c_int64]
         L.ref_guard_check.argtypes = [ctypes.c_uint64, ctypes.c_uint32, vp, ctypes.c_int64,
                                       vp, ctypes.c_int64, P(RefGuardResult)]
@@ -345,7 +345,8 @@ def merge_results(parts: Sequence[Dict]) -> Dict:
 
 def cosine_segment(dtype: str, rows: int, cols: int, stride_a: int, stride_b: int,
                    a: np.ndarray, b: np.ndarray, a_off: int = 0, b_off: int = 0) -> Dict:
-    """Cosine term of Eq. 1 in the defined reduction order (see ref_oracle.h)."""
+    """Cosine term of Eq. 1 from the exact sums, each rounded once (see
+    ref_oracle.h); also sum_abs_ab, the scale of other orders' error bounds."""
     seg = RefSeg(DTYPE[dtype], MODE["bitwise"], 0, 0, rows, cols, stride_a, stride_b, 0.0, 0.0)
     res = RefCosResult()
     a = np.ascontiguousarray(a).view(np.uint8)
@@ -357,8 +358,8 @@ def cosine_segment(dtype: str, rows: int, cols: int, stride_a: int, stride_b: in
 
 
 def cosine_nd(dtype: str, parts: Sequence, a: np.ndarray, b: np.ndarray) -> Dict:
-    """Cosine term of one result over N-D segments in the walk order (see
-    ref_oracle.h).  parts: (shape, stride_a, stride_b, a_off, b_off) per
+    """Cosine term of one result over the elements of N-D segments, from the
+    exact sums (see ref_oracle.h).  parts: (shape, stride_a, stride_b, a_off, b_off) per
     segment, in segment order; strides in elements, offsets in bytes of the
     uint8 arrays a and b."""
     n = len(parts)
@@ -381,9 +382,10 @@ def cosine_nd(dtype: str, parts: Sequence, a: np.ndarray, b: np.ndarray) -> Dict
     return res.as_dict()
 
 
-def pairwise_tree(x: np.ndarray) -> float:
+def exact_sum(x: np.ndarray) -> float:
+    """The float64 values of x summed exactly, rounded once to nearest (ties to even)."""
     x = np.ascontiguousarray(x, dtype=np.float64)
-    return float(lib().ref_pairwise_tree(_ptr(x) if x.size else None, x.size))
+    return float(lib().ref_exact_sum(_ptr(x) if x.size else None, x.size))
 
 
 def cosine_workload(w, cand: np.ndarray, ref: np.ndarray, threads: int = 1) -> List[Dict]:

@@ -24,11 +24,16 @@
  *  Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3"
  *  (SC'11).
  *
+ *  The cosine term of Eq. 1 has no summation order in its definition, so
+ *  its three sums are computed exactly (a fixed-point accumulator) and each
+ *  is rounded once.
+ *
  * Pins (tests/test_oracle_*.py): Philox known-answer vectors; codecs against
  * numpy/torch casts over every 8- and 16-bit pattern; the tolerance mask
  * against numpy.isclose; the fill's ln/sin/cos against libm; closed-form
  * counts of constructed cases; brute force over every (index, bit) of tiny
- * buffers and every byte of tiny guards.
+ * buffers and every byte of tiny guards; the exact sums against Python's
+ * exact rationals and math.fsum; the region copy against numpy slices.
  */
 #include "ref_oracle.h"
 
@@ -673,260 +678,218 @@ int ref_diff_segment_nd(const ref_seg_nd* seg, const uint8_t* a, const uint8_t* 
 }
 
 /* ------------------------------------------------------------------------ */
-/* Cosine term of Eq. 1: c = cos(K'(x), O(x)).  The products of two values   */
-/* of any of the float element types are exact in fp64, so every rounding    */
-/* below is an addition, taken in this defined order.                        */
+/* Cosine term of Eq. 1: c = cos(K'(x), O(x)) = sum a*b / (|a| * |b|) over  */
+/* the element pairs of a buffer with both values finite.  The definition   */
+/* fixes no order of summation, so the oracle computes each of the three    */
+/* sums exactly and rounds it once (to nearest, ties to even).  Every       */
+/* product is exact in fp64: the float element types have at most 24        */
+/* significant bits and exponents in [-149, 127], so a product has at most  */
+/* 48 significant bits and lies in [2^-298, 2^256].                         */
 /* ------------------------------------------------------------------------ */
 
-/* Left-complete pairwise tree: P(x[0..n)) = x[0] for n = 1, otherwise
- * P(x[0..h)) + P(x[h..n)) with h the largest power of two below n. */
-double ref_pairwise_tree(const double* x, int64_t n) {
-  if (n <= 0) return 0.0;
-  if (n == 1) return x[0];
-  int64_t h = 1;
-  while (h * 2 < n) h *= 2;
-  double left = ref_pairwise_tree(x, h);
-  double right = ref_pairwise_tree(x + h, n - h);
-  return left + right;
+/* The exact sum is a signed fixed-point integer with one bit for every power
+ * of two a binary64 value can carry: bit 0 weighs 2^-1074 (the smallest
+ * subnormal), the largest finite value ends below bit 2098, and 64 more bits
+ * leave room for 2^64 terms.  It is held as base-2^32 digits in int64, so an
+ * addition changes at most three digits by less than 2^32 each and no carry
+ * has to move until 2^30 additions have been made. */
+void ref_xacc_init(ref_xacc* x) { memset(x, 0, sizeof(*x)); }
+
+/* floor(v / 2^32) for any int64 v, without relying on how C shifts a
+ * negative value */
+static int64_t floor_div_2p32(int64_t v) {
+  const int64_t q = v / 4294967296LL;           /* truncates toward zero */
+  return (v < 0 && q * 4294967296LL != v) ? q - 1 : q;
 }
 
-int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res) {
-  int es = ref_esize(seg->dtype);
-  if (es == 0) return -1;
-  res->sum_ab = 0.0;
-  res->sum_aa = 0.0;
-  res->sum_bb = 0.0;
-  res->cosine = NAN;
-  res->pairs = 0;
-  res->blocks = 0;
-  if (!is_float(seg->dtype)) return 0;       /* not defined for integer buffers */
-  int64_t rows = seg->rows, cols = seg->cols;
-  if (rows <= 0 || cols <= 0) {
-    rows = 0;
-  } else if (rows == 1 || (seg->stride_a == cols && seg->stride_b == cols)) {
-    cols = rows * cols;                       /* one contiguous row */
-    rows = 1;
+/* Moves every digit's excess into the next one: digits 0..N-2 end in
+ * [0, 2^32) and the top digit carries the sign. */
+static void xacc_carry(ref_xacc* x) {
+  for (int i = 0; i + 1 < REF_XACC_DIGITS; ++i) {
+    const int64_t c = floor_div_2p32(x->d[i]);
+    x->d[i] -= c * 4294967296LL;
+    x->d[i + 1] += c;
   }
-  int64_t per_block = 4096 / es;              /* elements of a 4096-byte block */
-  int64_t per_chunk = 16 / es;                /* elements of a 16-byte chunk */
-  int64_t blocks_per_row = rows ? (cols + per_block - 1) / per_block : 0;
-  int64_t nblocks = rows * blocks_per_row;
-  double* bab = (double*)malloc(sizeof(double) * (size_t)(nblocks ? nblocks : 1) * 3);
-  if (!bab) return -1;
-  double* baa = bab + nblocks;
-  double* bbb = baa + nblocks;
-  int64_t k = 0;
-  for (int64_t r = 0; r < rows; ++r) {
-    for (int64_t blk = 0; blk < blocks_per_row; ++blk, ++k) {
-      double lab[64], laa[64], lbb[64];
-      for (int L = 0; L < 64; ++L) lab[L] = laa[L] = lbb[L] = 0.0;
-      int64_t c0 = blk * per_block;
-      int64_t len = cols - c0 < per_block ? cols - c0 : per_block;
-      for (int64_t t = 0; t < len; ++t) {
-        int64_t c = c0 + t;
-        uint64_t ra = load_raw(a + (r * seg->stride_a + c) * es, es);
-        uint64_t rb = load_raw(b + (r * seg->stride_b + c) * es, es);
-        double A, B;
-        if (ref_decode(seg->dtype, ra, &A) != 0 || ref_decode(seg->dtype, rb, &B) != 0) continue;
-        int L = (int)((t / per_chunk) % 64);
-        lab[L] = lab[L] + A * B;
-        laa[L] = laa[L] + A * A;
-        lbb[L] = lbb[L] + B * B;
-        res->pairs += 1;
-      }
-      /* xor butterfly over the 64 lanes */
-      for (int m = 32; m >= 1; m /= 2) {
-        double nab[64], naa[64], nbb[64];
-        for (int L = 0; L < 64; ++L) {
-          nab[L] = lab[L] + lab[L ^ m];
-          naa[L] = laa[L] + laa[L ^ m];
-          nbb[L] = lbb[L] + lbb[L ^ m];
-        }
-        for (int L = 0; L < 64; ++L) {
-          lab[L] = nab[L];
-          laa[L] = naa[L];
-          lbb[L] = nbb[L];
-        }
-      }
-      bab[k] = lab[0];
-      baa[k] = laa[0];
-      bbb[k] = lbb[0];
-    }
-  }
-  res->blocks = (uint64_t)nblocks;
-  res->sum_ab = ref_pairwise_tree(bab, nblocks);
-  res->sum_aa = ref_pairwise_tree(baa, nblocks);
-  res->sum_bb = ref_pairwise_tree(bbb, nblocks);
-  free(bab);
-  if (res->sum_aa == 0.0 && res->sum_bb == 0.0) {
-    res->cosine = 1.0;                        /* both vectors are zero */
-  } else if (res->sum_aa == 0.0 || res->sum_bb == 0.0) {
-    res->cosine = 0.0;                        /* exactly one is zero */
+  x->adds = 0;
+}
+
+/* Adds a finite binary64 value exactly.  From its IEEE 754 encoding: a normal
+ * value with biased exponent E >= 1 and fraction F is (2^52 + F) * 2^(E-1075),
+ * i.e. the integer 2^52 + F placed at bit E - 1 of the accumulator; a
+ * subnormal one (E = 0) is F * 2^-1074, i.e. F at bit 0. */
+void ref_xacc_add(ref_xacc* x, double v) {
+  uint64_t bits;
+  memcpy(&bits, &v, sizeof(bits));
+  const int neg = (int)(bits >> 63);
+  const int E = (int)((bits >> 52) & 0x7FF);
+  const uint64_t F = bits & 0xFFFFFFFFFFFFFull;
+  if (E == 0x7FF) return;                       /* not finite: callers never pass one */
+  const uint64_t m = E == 0 ? F : (F | (1ull << 52));
+  if (m == 0) return;
+  const int p = E == 0 ? 0 : E - 1;             /* bit position of m's bit 0 */
+  const unsigned __int128 w = (unsigned __int128)m << (p % 32);   /* below 2^85 */
+  const int k = p / 32;
+  const int64_t d0 = (int64_t)(uint32_t)w;
+  const int64_t d1 = (int64_t)(uint32_t)(w >> 32);
+  const int64_t d2 = (int64_t)(uint32_t)(w >> 64);
+  if (neg) {
+    x->d[k] -= d0;
+    x->d[k + 1] -= d1;
+    x->d[k + 2] -= d2;
   } else {
-    double na = sqrt(res->sum_aa);
-    double nb = sqrt(res->sum_bb);
-    double den = na * nb;
-    res->cosine = res->sum_ab / den;
+    x->d[k] += d0;
+    x->d[k + 1] += d1;
+    x->d[k + 2] += d2;
   }
-  return 0;
+  if (++x->adds >= (1LL << 30)) xacc_carry(x);
 }
 
-/* The walk of an N-D segment: dimensions of extent > 1, stably ordered by
- * decreasing stride of a (a stride of 0 counts as the largest), ties by
- * decreasing stride of b; then, from the innermost, a dimension that steps
- * exactly over the whole of the next-inner one in both operands is merged
- * into it.  Returns the merged dimensions, outermost first (at least one). */
+/* Bit i of a non-negative normalised accumulator. */
+static int xacc_bit(const ref_xacc* x, int i) { return (int)((x->d[i / 32] >> (i % 32)) & 1); }
+
+/* The binary64 value nearest to the exact sum, ties to even; an exact zero
+ * gives +0.0. */
+double ref_xacc_round(const ref_xacc* in) {
+  ref_xacc x = *in;
+  xacc_carry(&x);
+  const int neg = x.d[REF_XACC_DIGITS - 1] < 0;
+  if (neg) {                                    /* work with the magnitude */
+    for (int i = 0; i < REF_XACC_DIGITS; ++i) x.d[i] = -x.d[i];
+    xacc_carry(&x);
+  }
+  int top = -1;                                 /* highest set bit */
+  for (int i = REF_XACC_DIGITS * 32 - 1; i >= 0 && top < 0; --i)
+    if (xacc_bit(&x, i)) top = i;
+  if (top < 0) return 0.0;
+  double r;
+  if (top < 53) {                               /* at most 53 bits above 2^-1074: exact */
+    uint64_t m = 0;
+    for (int i = top; i >= 0; --i) m = (m << 1) | (uint64_t)xacc_bit(&x, i);
+    r = ldexp((double)m, -1074);
+  } else {
+    uint64_t m = 0;                             /* the 53 leading bits */
+    for (int i = top; i > top - 53; --i) m = (m << 1) | (uint64_t)xacc_bit(&x, i);
+    const int round = xacc_bit(&x, top - 53);
+    int sticky = 0;
+    for (int i = top - 54; i >= 0 && !sticky; --i) sticky = xacc_bit(&x, i);
+    int e = top - 52 - 1074;                    /* weight of m's last bit */
+    if (round && (sticky || (m & 1))) {
+      m += 1;
+      if (m == (1ull << 53)) {
+        m >>= 1;
+        e += 1;
+      }
+    }
+    r = ldexp((double)m, e);                    /* +Inf beyond the largest finite value */
+  }
+  return neg ? -r : r;
+}
+
+double ref_exact_sum(const double* v, int64_t n) {
+  ref_xacc x;
+  ref_xacc_init(&x);
+  for (int64_t k = 0; k < n; ++k) ref_xacc_add(&x, v[k]);
+  return ref_xacc_round(&x);
+}
+
+/* Exact running sums of one cosine term. */
 typedef struct {
-  int64_t n, sa, sb;
-} walk_dim;
+  ref_xacc ab, aa, bb, abs_ab;
+  uint64_t pairs;
+} cos_sums;
 
-static int64_t stride_key(int64_t v) { return v == 0 ? INT64_MAX : v; }
-
-static int walk_of(const ref_seg_nd* seg, walk_dim* out) {
-  walk_dim d[REF_MAX_DIMS];
-  int nd = 0;
-  for (int k = 0; k < seg->ndim; ++k) {
-    if (seg->shape[k] <= 1) continue;
-    walk_dim v = {seg->shape[k], seg->stride_a[k], seg->stride_b[k]};
-    int j = nd++;
-    /* insertion: v goes before every earlier entry it orders before */
-    while (j > 0) {
-      walk_dim u = d[j - 1];
-      int before = stride_key(v.sa) != stride_key(u.sa) ? stride_key(v.sa) > stride_key(u.sa)
-                                                         : stride_key(v.sb) > stride_key(u.sb);
-      if (!before) break;
-      d[j] = u;
-      --j;
-    }
-    d[j] = v;
-  }
-  walk_dim m[REF_MAX_DIMS];
-  int nm = 0;
-  for (int k = nd - 1; k >= 0; --k) {
-    if (nm > 0 && d[k].sa == m[nm - 1].n * m[nm - 1].sa && d[k].sb == m[nm - 1].n * m[nm - 1].sb)
-      m[nm - 1].n *= d[k].n;
-    else
-      m[nm++] = d[k];
-  }
-  if (nm == 0) {
-    m[0].n = 1;
-    m[0].sa = 1;
-    m[0].sb = 1;
-    nm = 1;
-  }
-  for (int k = 0; k < nm; ++k) out[k] = m[nm - 1 - k];
-  return nm;
+static void cos_sums_init(cos_sums* s) {
+  ref_xacc_init(&s->ab);
+  ref_xacc_init(&s->aa);
+  ref_xacc_init(&s->bb);
+  ref_xacc_init(&s->abs_ab);
+  s->pairs = 0;
 }
 
-/* Block sums of one row of len elements, element t at a + t*step_a and
- * b + t*step_b (bytes), appended at bab/baa/bbb[*k]. */
-static void row_block_sums(int32_t dtype, int es, const uint8_t* a, const uint8_t* b, int64_t step_a,
-                           int64_t step_b, int64_t len, double* bab, double* baa, double* bbb, int64_t* k,
-                           uint64_t* pairs) {
-  int64_t per_block = 4096 / es, per_chunk = 16 / es;
-  for (int64_t c0 = 0; c0 < len; c0 += per_block, ++*k) {
-    double lab[64], laa[64], lbb[64];
-    for (int L = 0; L < 64; ++L) lab[L] = laa[L] = lbb[L] = 0.0;
-    int64_t n = len - c0 < per_block ? len - c0 : per_block;
-    for (int64_t t = 0; t < n; ++t) {
-      uint64_t ra = load_raw(a + (c0 + t) * step_a, es);
-      uint64_t rb = load_raw(b + (c0 + t) * step_b, es);
-      double A, B;
-      if (ref_decode(dtype, ra, &A) != 0 || ref_decode(dtype, rb, &B) != 0) continue;
-      int L = (int)((t / per_chunk) % 64);
-      lab[L] = lab[L] + A * B;
-      laa[L] = laa[L] + A * A;
-      lbb[L] = lbb[L] + B * B;
-      *pairs += 1;
-    }
-    for (int m = 32; m >= 1; m /= 2) {
-      double nab[64], naa[64], nbb[64];
-      for (int L = 0; L < 64; ++L) {
-        nab[L] = lab[L] + lab[L ^ m];
-        naa[L] = laa[L] + laa[L ^ m];
-        nbb[L] = lbb[L] + lbb[L ^ m];
-      }
-      for (int L = 0; L < 64; ++L) {
-        lab[L] = nab[L];
-        laa[L] = naa[L];
-        lbb[L] = nbb[L];
-      }
-    }
-    bab[*k] = lab[0];
-    baa[*k] = laa[0];
-    bbb[*k] = lbb[0];
-  }
+/* One element pair: excluded when either value is NaN or infinite. */
+static void cos_pair(int32_t dtype, uint64_t ra, uint64_t rb, cos_sums* s) {
+  double A, B;
+  if (ref_decode(dtype, ra, &A) != 0 || ref_decode(dtype, rb, &B) != 0) return;
+  ref_xacc_add(&s->ab, A * B);
+  ref_xacc_add(&s->aa, A * A);
+  ref_xacc_add(&s->bb, B * B);
+  ref_xacc_add(&s->abs_ab, fabs(A * B));
+  s->pairs += 1;
 }
 
-int ref_cosine_nd(const ref_seg_nd* segs, int32_t n, const uint8_t* const* a, const uint8_t* const* b,
-                  ref_cos_result* res) {
-  res->sum_ab = res->sum_aa = res->sum_bb = 0.0;
-  res->cosine = NAN;
-  res->pairs = 0;
-  res->blocks = 0;
-  if (n <= 0) {
-    res->cosine = 1.0;                        /* no elements: both sums of squares are 0 */
-    return 0;
-  }
-  int32_t dtype = segs[0].dtype;
-  int es = ref_esize(dtype);
-  if (es == 0) return -1;
-  for (int32_t s = 0; s < n; ++s)
-    if (segs[s].dtype != dtype || segs[s].ndim < 0 || segs[s].ndim > REF_MAX_DIMS) return -1;
-  if (!is_float(dtype)) return 0;
-  /* first pass: blocks of every row of every segment */
-  int64_t nblocks = 0;
-  for (int32_t s = 0; s < n; ++s) {
-    int empty = 0;
-    for (int d = 0; d < segs[s].ndim; ++d) empty |= segs[s].shape[d] == 0;
-    if (empty) continue;
-    walk_dim w[REF_MAX_DIMS];
-    int nw = walk_of(&segs[s], w);
-    int64_t rows = 1;
-    for (int d = 0; d + 1 < nw; ++d) rows *= w[d].n;
-    nblocks += rows * ((w[nw - 1].n + 4096 / es - 1) / (4096 / es));
-  }
-  double* bab = (double*)malloc(sizeof(double) * (size_t)(nblocks ? nblocks : 1) * 3);
-  if (!bab) return -1;
-  double* baa = bab + nblocks;
-  double* bbb = baa + nblocks;
-  int64_t k = 0;
-  for (int32_t s = 0; s < n; ++s) {
-    int empty = 0;
-    for (int d = 0; d < segs[s].ndim; ++d) empty |= segs[s].shape[d] == 0;
-    if (empty) continue;
-    walk_dim w[REF_MAX_DIMS];
-    int nw = walk_of(&segs[s], w);
-    int64_t rows = 1;
-    for (int d = 0; d + 1 < nw; ++d) rows *= w[d].n;
-    for (int64_t r = 0; r < rows; ++r) {
-      /* outer walk index of row r, last outer dimension fastest */
-      int64_t rest = r, off_a = 0, off_b = 0;
-      for (int d = nw - 2; d >= 0; --d) {
-        int64_t idx = rest % w[d].n;
-        rest /= w[d].n;
-        off_a += idx * w[d].sa;
-        off_b += idx * w[d].sb;
-      }
-      row_block_sums(dtype, es, a[s] + off_a * es, b[s] + off_b * es, w[nw - 1].sa * es, w[nw - 1].sb * es,
-                     w[nw - 1].n, bab, baa, bbb, &k, &res->pairs);
-    }
-  }
-  res->blocks = (uint64_t)nblocks;
-  res->sum_ab = ref_pairwise_tree(bab, nblocks);
-  res->sum_aa = ref_pairwise_tree(baa, nblocks);
-  res->sum_bb = ref_pairwise_tree(bbb, nblocks);
-  free(bab);
+/* c = S_ab / (sqrt(S_aa) * sqrt(S_bb)) from the rounded sums, each operation
+ * rounded; 1 when both vectors are zero, 0 when exactly one is. */
+static void cos_finish(const cos_sums* s, ref_cos_result* res) {
+  res->sum_ab = ref_xacc_round(&s->ab);
+  res->sum_aa = ref_xacc_round(&s->aa);
+  res->sum_bb = ref_xacc_round(&s->bb);
+  res->sum_abs_ab = ref_xacc_round(&s->abs_ab);
+  res->pairs = s->pairs;
   if (res->sum_aa == 0.0 && res->sum_bb == 0.0) {
     res->cosine = 1.0;
   } else if (res->sum_aa == 0.0 || res->sum_bb == 0.0) {
     res->cosine = 0.0;
   } else {
-    double na = sqrt(res->sum_aa);
-    double nb = sqrt(res->sum_bb);
-    double den = na * nb;
+    const double na = sqrt(res->sum_aa);
+    const double nb = sqrt(res->sum_bb);
+    const double den = na * nb;
     res->cosine = res->sum_ab / den;
   }
+}
+
+static void cos_undefined(ref_cos_result* res) {
+  res->sum_ab = res->sum_aa = res->sum_bb = res->sum_abs_ab = 0.0;
+  res->cosine = NAN;                            /* not defined for integer buffers */
+  res->pairs = 0;
+}
+
+int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res) {
+  const int es = ref_esize(seg->dtype);
+  if (es == 0) return -1;
+  cos_undefined(res);
+  if (!is_float(seg->dtype)) return 0;
+  cos_sums s;
+  cos_sums_init(&s);
+  for (int64_t r = 0; r < seg->rows && seg->cols > 0; ++r)
+    for (int64_t c = 0; c < seg->cols; ++c)
+      cos_pair(seg->dtype, load_raw(a + (r * seg->stride_a + c) * es, es),
+               load_raw(b + (r * seg->stride_b + c) * es, es), &s);
+  cos_finish(&s, res);
+  return 0;
+}
+
+int ref_cosine_nd(const ref_seg_nd* segs, int32_t n, const uint8_t* const* a, const uint8_t* const* b,
+                  ref_cos_result* res) {
+  cos_undefined(res);
+  if (n <= 0) {
+    res->cosine = 1.0;                          /* no elements: both vectors are zero */
+    res->sum_ab = res->sum_aa = res->sum_bb = res->sum_abs_ab = 0.0;
+    return 0;
+  }
+  const int32_t dtype = segs[0].dtype;
+  const int es = ref_esize(dtype);
+  if (es == 0) return -1;
+  for (int32_t k = 0; k < n; ++k)
+    if (segs[k].dtype != dtype || segs[k].ndim < 0 || segs[k].ndim > REF_MAX_DIMS) return -1;
+  if (!is_float(dtype)) return 0;
+  cos_sums s;
+  cos_sums_init(&s);
+  for (int32_t k = 0; k < n; ++k) {
+    const ref_seg_nd* seg = &segs[k];
+    int64_t count = 1;
+    for (int d = 0; d < seg->ndim; ++d) count *= seg->shape[d];
+    for (int64_t i = 0; i < count; ++i) {       /* logical order; any order gives the same sums */
+      int64_t rest = i, off_a = 0, off_b = 0;
+      for (int d = seg->ndim - 1; d >= 0; --d) {
+        const int64_t idx = rest % seg->shape[d];
+        rest /= seg->shape[d];
+        off_a += idx * seg->stride_a[d];
+        off_b += idx * seg->stride_b[d];
+      }
+      cos_pair(dtype, load_raw(a[k] + off_a * es, es), load_raw(b[k] + off_b * es, es), &s);
+    }
+  }
+  cos_finish(&s, res);
   return 0;
 }
 

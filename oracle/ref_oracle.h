@@ -128,29 +128,36 @@ int ref_guard_check(uint64_t seed, uint32_t alloc_id, const uint8_t* lo, int64_t
  * first_bad_pad of `res` only. */
 int ref_pad_check(const ref_alloc* A, uint64_t seed, const uint8_t* data, ref_guard_result* res);
 
-/* Cosine term of Eq. 1 over one segment (float dtypes).  sum_* are fp64
- * sums over the pairs with both values finite, in the defined order: rows
- * (a segment contiguous in both operands is one row), 4096-byte blocks of a
- * row, 64 lanes per block taking every 64th 16-byte chunk, an xor butterfly
- * over the lanes, and a left-complete pairwise tree over the blocks. */
+/* Exact sum of binary64 values: a fixed-point integer from 2^-1074 up, in
+ * base-2^32 digits held in int64 (a carry is needed only every 2^30
+ * additions), rounded once to the nearest binary64 value, ties to even. */
+#define REF_XACC_DIGITS 70          /* 2240 bits: 2^-1074 .. 2^1024, 64 bits of headroom, sign */
+typedef struct {
+  int64_t d[REF_XACC_DIGITS];
+  int64_t adds;                     /* additions since the last carry */
+} ref_xacc;
+void ref_xacc_init(ref_xacc* x);
+void ref_xacc_add(ref_xacc* x, double v);      /* v finite */
+double ref_xacc_round(const ref_xacc* x);
+double ref_exact_sum(const double* v, int64_t n);
+
+/* Cosine term of Eq. 1 over one segment (float dtypes): the sums over the
+ * element pairs with both values finite, each computed exactly and rounded
+ * once; cosine = sum_ab / (sqrt(sum_aa) * sqrt(sum_bb)), each operation
+ * rounded (1 when both sums of squares are 0, 0 when exactly one is).
+ * sum_abs_ab = sum |a*b| (rounded once), the scale of the error bound of any
+ * other summation order.  Integer buffers: sums 0, cosine NaN. */
 typedef struct {
   double sum_ab, sum_aa, sum_bb, cosine;
   uint64_t pairs;        /* pairs with both values finite */
-  uint64_t blocks;
+  double sum_abs_ab;
 } ref_cos_result;
 int ref_cosine_segment(const ref_seg* seg, const uint8_t* a, const uint8_t* b, ref_cos_result* res);
-/* The same term over n N-D segments that share one result, in the walk
- * order: in each segment the dimensions of extent > 1 are ordered by
- * decreasing stride of a (stride 0 first), ties by decreasing stride of b,
- * then neighbours contiguous in both operands are merged; the innermost
- * merged dimension forms rows, the others order them (last fastest); rows are
- * cut into blocks as above, and the blocks of all n segments, in segment
- * order, combine by the pairwise tree.  a[k], b[k]: element (0, ..., 0) of
- * segment k.  Every segment must have the same float dtype. */
+/* The same term over the elements of n N-D segments that share one result.
+ * a[k], b[k]: element (0, ..., 0) of segment k.  Every segment must have the
+ * same dtype.  n = 0: cosine 1 over no pairs. */
 int ref_cosine_nd(const ref_seg_nd* segs, int32_t n, const uint8_t* const* a, const uint8_t* const* b,
                   ref_cos_result* res);
-/* the left-complete pairwise tree alone (exposed for its pins) */
-double ref_pairwise_tree(const double* x, int64_t n);
 
 /* Restore / snapshot of captured regions: dst[k][0..bytes) = src[k][0..bytes)
  * for each region, in order (regions are host memory here). */

@@ -84,3 +84,66 @@ def check_fill_sampled(w, st, variant_of_side, rng, n_random=16, width=4096):
                 got = st.alloc_bytes(side, k, s, n)
                 want = P.fill_range(k, variant, s, n)
                 assert_bytes_equal(got, want, f"{side} alloc {k} bytes [{s}, {s + n})")
+
+
+# ------------------------------------------------------------ the cosine term
+U = 2.0 ** -53
+
+
+def gamma(k: int) -> float:
+    """gamma_k = k u / (1 - k u): the relative error bound of k roundings."""
+    return k * U / (1.0 - k * U)
+
+
+def cosine_depth(dtype: str, blocks: int) -> int:
+    """Roundings on one product's path through the library's documented order:
+    the lane's run of 4 chunks, 6 butterfly steps, the block tree's depth,
+    and one more for the oracle's own rounding of the exact sum."""
+    import cosine_order
+    return cosine_order.lane_terms(dtype) + 6 + max(1, blocks - 1).bit_length() + 1
+
+
+def assert_cosine(got, exact, model, dtypes, what=""):
+    """The GPU's cosine results against (1) the documented-order model, bit for
+    bit on every field (the library's reproducibility promise), and (2) the
+    oracle's exact sums, within the error bound of that order: |s - S| <=
+    gamma_D * sum|t| for each sum, 2.5 gamma_D + 16u for the cosine (the three
+    sums' errors through one division, two square roots and a product), and
+    the pair count exactly."""
+    import math
+    assert len(got) == len(exact) == len(model) == len(dtypes), what
+    for k, (g, e, m, dt) in enumerate(zip(got, exact, model, dtypes)):
+        for f in m:
+            assert bits(g[f]) == bits(m[f]), f"{what} entry {k} field {f}: gpu {g[f]!r} order model {m[f]!r}"
+        assert g["pairs"] == e["pairs"], f"{what} entry {k}: pairs gpu {g['pairs']} oracle {e['pairs']}"
+        if math.isnan(e["cosine"]):
+            assert math.isnan(g["cosine"]) and g["sum_ab"] == g["sum_aa"] == g["sum_bb"] == 0.0, f"{what} {k}"
+            continue
+        gd = gamma(cosine_depth(dt, g["blocks"]))
+        for f, scale in (("sum_ab", e["sum_abs_ab"]), ("sum_aa", e["sum_aa"]), ("sum_bb", e["sum_bb"])):
+            assert abs(g[f] - e[f]) <= gd * scale, (
+                f"{what} entry {k} {f}: gpu {g[f]!r} exact {e[f]!r} bound {gd * scale!r}")
+        if e["sum_aa"] == 0.0 or e["sum_bb"] == 0.0:
+            assert g["cosine"] == e["cosine"], f"{what} entry {k} cosine {g['cosine']} vs {e['cosine']}"
+        else:
+            assert abs(g["cosine"] - e["cosine"]) <= 2.5 * gd + 16 * U, (
+                f"{what} entry {k} cosine: gpu {g['cosine']!r} exact {e['cosine']!r}")
+
+
+def cosine_expected(dtype, rows, cols, sa, sb, a, b, a_off=0, b_off=0):
+    """(oracle result from exact sums, documented-order model) of one 2-D segment."""
+    import cosine_order
+    return (oracle.cosine_segment(dtype, rows, cols, sa, sb, a, b, a_off, b_off),
+            cosine_order.cosine_2d(dtype, rows, cols, sa, sb, a, b, a_off, b_off))
+
+
+def cosine_workload_expected(w, cand, ref, threads=THREADS):
+    """Exact oracle results, order-model results and dtypes of every compare of w."""
+    from concurrent.futures import ThreadPoolExecutor
+    def one(c):
+        a = w.allocs[c.alloc]
+        off = w.data_offset(c.alloc)
+        return cosine_expected(a.dtype, a.rows, a.cols, a.stride, a.stride, cand, ref, off, off)
+    with ThreadPoolExecutor(threads) as ex:
+        pairs = list(ex.map(one, w.compares))
+    return [p[0] for p in pairs], [p[1] for p in pairs], [w.allocs[c.alloc].dtype for c in w.compares]

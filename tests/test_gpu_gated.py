@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import log
+from gpu_helpers import U, gamma, log
 from paper_2608_20711_amd.gated import candidates as C
 
 pytestmark = pytest.mark.gpu
@@ -133,7 +133,10 @@ def test_comparison_records_match_the_oracle(harness, name):
         assert got["max_abs"] == r["max_abs"], bname
         if tol:
             c = oracle.cosine_segment(names[dt], rows, cols, stride, stride, work, ref, off, off)
-            assert got["cosine"] == c["cosine"] or (math.isnan(got["cosine"]) and math.isnan(c["cosine"])), bname
+            if math.isnan(c["cosine"]):
+                assert math.isnan(got["cosine"]), bname
+            else:   # exact sums against the library's order: within its error bound
+                assert abs(got["cosine"] - c["cosine"]) <= 2.5 * gamma(110) + 16 * U, bname
         lo = work[x.offsets[k]:off]
         n = ((rows - 1) * stride + cols) * es
         hi = work[off + n:off + n + 4096]
