@@ -125,12 +125,13 @@ enum {
  *   [guard_lo bytes][data: rows rows of `stride` elements, the last row
  *   holding only `cols`][guard_hi bytes]
  * i.e. data bytes = ((rows - 1) * stride + cols) * element size (0 if rows
- * or cols is 0).  Requirements: base 16-byte aligned (fill) or non-null
- * (guard check); rows, cols >= 0; stride >= cols; guard_lo a multiple of the
- * element size; guard sizes >= 0.  `alloc_id` is the logical buffer id and
- * must be the same for the candidate's and the reference's copy of a buffer:
- * it keys the generator, so both copies get identical values, pads and
- * canaries.
+ * or cols is 0).  Requirements: base non-null and a multiple of the element
+ * size (an allocation that does not start on a 16-byte boundary is filled
+ * byte by byte, several times slower); rows, cols >= 0; stride >= cols;
+ * guard_lo a multiple of the element size; guard sizes >= 0.  `alloc_id` is
+ * the logical buffer id and must be the same for the candidate's and the
+ * reference's copy of a buffer: it keys the generator, so both copies get
+ * identical values, pads and canaries.
  */
 typedef struct {
   uint64_t base;
@@ -166,6 +167,9 @@ enum { ASMEVO_SIDE_CANDIDATE = 0, ASMEVO_SIDE_BOTH = 1 };
  * entries hit one element the last in the array wins, and element entries
  * override Bernoulli rules.  For a RATE rule `index` holds the threshold T
  * (0 <= T <= 2^32): element i is selected iff its SELECT draw is below T.
+ * The caller converts a rate r in [0, 1] into T; the rule this library's
+ * bindings use is T = floor(r * 2^32 + 1/2) (2^32 for r = 1), the same as
+ * the library applies to the rate p0 of ASMEVO_DIST_BOUNDARY.
  */
 typedef struct {
   uint32_t alloc;      /* index into the allocation array of the call */

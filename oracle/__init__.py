@@ -240,13 +240,14 @@ def ref_allocs(w) -> ctypes.Array:
 
 
 def ref_injections(w) -> ctypes.Array:
+    from workloads import rate_threshold
     arr = (RefInj * max(1, len(w.injections)))()
     for t, j in enumerate(w.injections):
         kind = KIND[j.kind]
         index = j.index
         if j.rate is not None:
             kind |= RATE
-            index = int(round(j.rate * 2.0 ** 32))
+            index = rate_threshold(j.rate)
         arg = j.arg & 0xFFFFFFFF
         arr[t] = RefInj(j.alloc, kind, SIDES[j.sides], arg, index, j.atol, j.rtol)
     return arr

@@ -135,7 +135,7 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
     const int es = esize_of(A.dtype);
     const uint64_t D = data_bytes(A);
     const uint64_t total = (uint64_t)A.guard_lo + D + (uint64_t)A.guard_hi;
-    if (total > 0 && (A.base == 0 || (A.base & 15u) != 0)) return ASMEVO_E_INVALID;
+    if (total > 0 && (A.base == 0 || A.base % (uint64_t)es != 0)) return ASMEVO_E_INVALID;
     if ((A.flags & ~ASMEVO_FILL_SATURATE) != 0) return ASMEVO_E_INVALID;
     switch (A.dist) {
       case ASMEVO_DIST_NORMAL:
@@ -177,7 +177,8 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
     F.alloc_id = A.alloc_id;
     F.dist = A.dist;
     F.saturate = (A.flags & ASMEVO_FILL_SATURATE) ? 1u : 0u;
-    const uint64_t chunks = (total + kChunk - 1) / kChunk;
+    F.phase = (uint32_t)(A.base % kChunk);
+    const uint64_t chunks = (F.phase + total + kChunk - 1) / kChunk;   // 16-byte blocks of memory touched
     tiles += (chunks + kWave - 1) / kWave;
     if (total) spans.emplace_back(A.base, A.base + total);
   }
@@ -285,12 +286,10 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
 
 namespace {
 
-// Validates the segments and builds their device descriptors.  `row_tiled`
-// keeps every tile inside one row (the cosine's 4096-byte blocks).
-asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled,
-                        std::vector<DiffSeg>& dev, uint64_t& tiles) {
+// Validates the segments and builds their device descriptors dev[0..n).
+// `row_tiled` keeps every tile inside one row (the cosine's 4096-byte blocks).
+asmevo_status plan_diff(const asmevo_segment* segs, int32_t n, bool row_tiled, DiffSeg* dev, uint64_t& tiles) {
   if (n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
-  dev.assign((size_t)n, DiffSeg{});
   tiles = 0;
   for (int32_t k = 0; k < n; ++k) {
     const asmevo_segment& S = segs[k];
@@ -616,9 +615,9 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
                                       size_t ws_bytes, void* stream, int32_t workgroups) {
   if (n < 0 || (n > 0 && (!segs || !results)) || workgroups < 0) return ASMEVO_E_INVALID;
   if (n == 0) return ASMEVO_OK;
-  std::vector<DiffSeg> dev;
+  std::vector<DiffSeg> dev((size_t)n);
   uint64_t tiles = 0;
-  asmevo_status st = plan_diff(segs, n, false, dev, tiles);
+  asmevo_status st = plan_diff(segs, n, false, dev.data(), tiles);
   if (st != ASMEVO_OK) return st;
   const size_t bytes = dev.size() * sizeof(DiffSeg);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
@@ -638,6 +637,7 @@ asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
                                    size_t ws_bytes, void* stream) {
   return asmevo_diff_segments_ex(segs, n, results, workspace, ws_bytes, stream, 0);
 }
+
 
 size_t asmevo_diff_nd_workspace_bytes(int32_t n) {
   const size_t m = n > 0 ? (size_t)n : 0;
@@ -672,9 +672,10 @@ asmevo_status asmevo_diff_segments_nd(const asmevo_segment_nd* segs, int32_t n,
 }
 
 size_t asmevo_diff_cosine_workspace_bytes(const asmevo_segment* segs, int32_t n) {
-  std::vector<DiffSeg> dev;
+  if (n <= 0 || !segs) return 0;
+  std::vector<DiffSeg> dev((size_t)n);
   uint64_t tiles = 0;
-  if (n <= 0 || plan_diff(segs, n, true, dev, tiles) != ASMEVO_OK) return 0;
+  if (plan_diff(segs, n, true, dev.data(), tiles) != ASMEVO_OK) return 0;
   return cos_plan(dev, tiles).bytes;
 }
 
@@ -683,9 +684,9 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
                                  void* workspace, size_t ws_bytes, void* stream) {
   if (n < 0 || (n > 0 && (!segs || !results || !cos_results))) return ASMEVO_E_INVALID;
   if (n == 0) return ASMEVO_OK;
-  std::vector<DiffSeg> dev;
+  std::vector<DiffSeg> dev((size_t)n);
   uint64_t tiles = 0;
-  asmevo_status st = plan_diff(segs, n, true, dev, tiles);
+  asmevo_status st = plan_diff(segs, n, true, dev.data(), tiles);
   if (st != ASMEVO_OK) return st;
   const CosPlan P = cos_plan(dev, tiles);
   for (const CosLevels& L : P.lv)     // the final fold stages at most 255 entries per level

@@ -337,8 +337,10 @@ __device__ __forceinline__ uint8_t canary_byte(uint32_t alloc_id, uint32_t side,
   return byte_of(stream(seed, alloc_id, kCanary, side, 0, p >> 4), (uint32_t)(p & 15u));
 }
 
-// Byte-by-byte general path for chunks that straddle a region boundary.
-__device__ __forceinline__ void general_chunk(const FillAlloc& A, const FillRule* rules, uint64_t o,
+// Byte-by-byte general path for chunks that straddle a region boundary or
+// the allocation's ends (o may be negative: the first chunk of an
+// allocation that does not start on a 16-byte boundary).
+__device__ __forceinline__ void general_chunk(const FillAlloc& A, const FillRule* rules, int64_t o,
                               uint64_t seed, uint32_t w[4]) {
   const uint64_t glo = A.guard_lo, D = A.data_bytes, tot = A.total_bytes;
   uint64_t cached_e = ~0ull, cached_v = 0;
@@ -346,7 +348,8 @@ __device__ __forceinline__ void general_chunk(const FillAlloc& A, const FillRule
   for (int k = 0; k < 4; ++k) w[k] = 0;
 #pragma unroll 1
   for (uint32_t b = 0; b < 16; ++b) {
-    const uint64_t p = o + b;
+    if (o + (int64_t)b < 0) continue;
+    const uint64_t p = (uint64_t)(o + (int64_t)b);
     if (p >= tot) break;
     uint8_t byte;
     if (p < glo) {
@@ -388,12 +391,20 @@ __device__ __forceinline__ bool try_data_chunk(const FillAlloc& A, const FillAll
   return true;
 }
 
+// Allocation bytes [o, o + 16) (one 16-byte block of memory; o may be
+// negative for the first one).  The whole-chunk paths below need the
+// allocation to start on a 16-byte boundary (phase 0), where a chunk is one
+// generator block of canary bytes or whole elements; otherwise every chunk
+// goes byte by byte.
 __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillAlloc* Ap, const FillRule* rules,
-                                               uint64_t o, uint64_t seed) {
+                                               int64_t os, uint64_t seed) {
   const uint64_t glo = A.guard_lo, D = A.data_bytes, tot = A.total_bytes;
+  const uint64_t o = (uint64_t)os;            // used only where os >= 0
   uint32_t w[4];
   bool done = false;
-  if (o + 16 <= glo) {
+  if (A.phase != 0) {
+    // (no whole-chunk path)
+  } else if (o + 16 <= glo) {
     const U4 C = stream(seed, A.alloc_id, kCanary, 0, 0, o >> 4);
     w[0] = C.x; w[1] = C.y; w[2] = C.z; w[3] = C.w;
     done = true;
@@ -412,14 +423,16 @@ __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillAll
       default: done = try_data_chunk<ASMEVO_U8>(A, Ap, rules, o, seed, w); break;
     }
   }
-  if (!done) general_chunk(A, rules, o, seed, w);
-  if (o + 16 <= tot) {
+  if (!done) general_chunk(A, rules, os, seed, w);
+  if (os >= 0 && o + 16 <= tot) {             // base + o is 16-byte aligned
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 v = {w[0], w[1], w[2], w[3]};
     *gptr_mut<u32x4>(A.base + o) = v;
-  } else {
-    AS_GLOBAL uint8_t* dst = gptr_mut<uint8_t>(A.base + o);
-    for (uint32_t b = 0; o + b < tot; ++b) dst[b] = (uint8_t)(w[b >> 2] >> (8u * (b & 3u)));
+  } else {                                    // only the allocation's own bytes
+    for (uint32_t b = 0; b < 16; ++b) {
+      const int64_t p = os + (int64_t)b;
+      if (p >= 0 && (uint64_t)p < tot) *gptr_mut<uint8_t>(A.base + (uint64_t)p) = (uint8_t)(w[b >> 2] >> (8u * (b & 3u)));
+    }
   }
 }
 
@@ -446,8 +459,10 @@ __global__ __launch_bounds__(kFillBlock) void fill_kernel(const FillAlloc* __res
   for (uint64_t t = wave; t < total_tiles; t += nwaves) {
     while (k + 1 < n && allocs[k + 1].tile_begin <= t) ++k;
     const FillAlloc A = allocs[k];
-    const uint64_t o = ((t - A.tile_begin) * kWave + lane) * kChunk;
-    if (o < A.total_bytes) fill_one_chunk(A, allocs + k, rules, o, seed);
+    // chunk c of the allocation is the 16-byte block of memory at
+    // base - phase + 16 c, i.e. allocation bytes [16 c - phase, 16 c - phase + 16)
+    const int64_t o = (int64_t)(((t - A.tile_begin) * kWave + lane) * kChunk) - (int64_t)A.phase;
+    if (o < (int64_t)A.total_bytes) fill_one_chunk(A, allocs + k, rules, o, seed);
   }
 }
 

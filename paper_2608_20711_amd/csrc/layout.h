@@ -117,7 +117,7 @@ constexpr int kMaxRules = 16;      // Bernoulli rules per allocation
 constexpr int kFillBlock = 256;
 
 struct FillAlloc {              // 128 bytes
-  uint64_t base;                // first lo-guard byte (16-byte aligned)
+  uint64_t base;                // first lo-guard byte (element-aligned)
   uint64_t total_bytes;         // guard_lo + data + guard_hi
   uint64_t guard_lo, data_bytes;
   uint64_t rows, cols, stride;  // elements
@@ -125,7 +125,8 @@ struct FillAlloc {              // 128 bytes
   double p0, p1;
   int64_t i0, i1;
   uint32_t dtype, esize, alloc_id, dist;
-  uint32_t saturate, rule_begin, rule_count, pad0;
+  uint32_t saturate, rule_begin, rule_count;
+  uint32_t phase;               // base mod 16: the chunks are the 16-byte blocks of memory
 };
 static_assert(sizeof(FillAlloc) == 128, "FillAlloc layout");
 

@@ -27,13 +27,14 @@ GUARD_RESULT_DTYPE = np.dtype([("bad_lo", "<u8"), ("bad_hi", "<u8"),
 
 
 def injection_structs(w) -> List[Injection]:
+    from workloads import rate_threshold
     out = []
     for j in w.injections:
         kind = KIND_CODE[j.kind]
         index = j.index
         if j.rate is not None:
             kind |= INJ_RATE
-            index = int(round(j.rate * 2.0 ** 32))
+            index = rate_threshold(j.rate)
         out.append(Injection(j.alloc, kind, SIDE_CODE[j.sides], j.arg & 0xFFFFFFFF, index, j.atol, j.rtol))
     return out
 

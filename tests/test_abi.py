@@ -116,7 +116,7 @@ def _inj(**kw):
 
 
 @pytest.mark.parametrize("allocs,inj,status", [
-    ([_alloc(base=0x100008)], [], lib.E_INVALID),                         # not 16-byte aligned
+    ([_alloc(base=0x100002)], [], lib.E_INVALID),                         # not element-aligned (f32)
     ([_alloc(base=0)], [], lib.E_INVALID),
     ([_alloc(dtype=0)], [], lib.E_INVALID),
     ([_alloc(stride=10)], [], lib.E_INVALID),
@@ -286,3 +286,4 @@ def test_diff_nd_ndim_and_workspace():
     with pytest.raises(lib.AsmevoError) as e:
         lib.diff_segments_nd([_seg_nd()], 0, 1, 0x50000, need, stream=0)
     assert e.value.status == lib.E_INVALID
+

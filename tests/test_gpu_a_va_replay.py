@@ -8,9 +8,10 @@ diffs the data each captured pointer points to (used as the segment address)
 against the snapshot.
 
 Explicit device addresses were honoured only while no other process held
-the device, so this test runs first among the GPU tests (the module name
-sorts first) and is skipped when the test process already uses the GPU, or
-when the capture process cannot map any of the candidate addresses."""
+the device, so this test runs before every other test of a session
+(tests/conftest.py moves it to the front whatever the selection or order)
+and is skipped when the test process already uses the GPU, or when the
+capture process cannot map any of the candidate addresses."""
 import json
 import os
 import subprocess
@@ -89,19 +90,6 @@ print(json.dumps({"addr": got, "in_range": bool(((ptrs[:256] >= got) & (ptrs[:25
                   "control": int(raw["bitwise_mismatches"][256])}), flush=True)
 lib.va_free(got)
 """
-
-
-def _child(src, *args):
-    import json
-    import os
-    import subprocess
-    import sys
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    out = subprocess.run([sys.executable, "-c", src, *map(str, args)], capture_output=True, text=True,
-                         timeout=240, cwd=root)
-    assert out.returncode == 0, out.stderr[-2000:]
-    return json.loads(out.stdout.strip().splitlines()[-1])
-
 
 
 def _child(src, *args):

@@ -303,3 +303,55 @@ def test_every_narrow_row_width(dtype):
     raw = res.cpu().numpy().view(SEG_RESULT_DTYPE)
     got_nd = [{f: raw[f][k].item() for f in SEG_RESULT_DTYPE.names} for k in range(len(segs))]
     assert_results_equal(got_nd, want, f"{dtype} narrow N-D")
+
+
+def test_fill_element_aligned_bases():
+    """Allocations that start at every element-aligned phase of a 16-byte
+    block (the fill then goes byte by byte): every allocation byte equals the
+    oracle's fill, the bytes between allocations are never written, and the
+    guard check and the diff over those allocations match the oracle."""
+    specs = []
+    for dt in ("f32", "bf16", "f16", "fp8e4m3", "i32", "i64", "u8"):
+        es = ESIZE[dt]
+        for phase in range(es, 16, es):
+            specs.append((dt, phase))
+    allocs, offsets, inj = [], [], []
+    dists = {"f32": ("normal", {}), "bf16": ("boundary", dict(p0=0.2, p1=3.0)), "f16": ("normal", {}),
+             "fp8e4m3": ("normal", dict(p1=50.0)), "i32": ("uniform_int", dict(i0=-9, i1=1000)),
+             "i64": ("bits", {}), "u8": ("bits", {})}
+    for k, (dt, phase) in enumerate(specs):
+        es = ESIZE[dt]
+        rows = 1 + k % 4
+        cols = 5 + 3 * k % 37
+        stride = cols + (k % 3)
+        glo = es * (k % 5)
+        ghi = 3 * (k % 4)
+        dist, kw = dists[dt]
+        allocs.append(Alloc(k, dt, rows, cols, stride, glo, ghi, dist, **kw))
+        offsets.append(1024 * k + phase)
+        inj.append(Injection(k, "flip_bit", arg=-1, rate=0.3))
+        if ghi:
+            inj.append(Injection(k, "guard_write_hi", arg=1, index=ghi - 1))
+    compares = [Compare(k, "tolerance" if a.dtype in ("f32", "bf16", "f16", "fp8e4m3") else "bitwise",
+                        "equal", 1e-3, 1e-3) for k, a in enumerate(allocs)]
+    w = Workload("phases", "", 0x5EED, allocs, inj, compares, offsets=offsets, arena_bytes=1024 * len(specs))
+    assert all(offsets[k] + a.total_bytes <= 1024 * (k + 1) for k, a in enumerate(allocs))
+    log(f"[phases] {len(allocs)} allocations")
+    st = DeviceState(w)
+    st.ref.fill_(0xA5)
+    st.cand.fill_(0xA5)
+    st.fill("ref", 0)
+    st.fill("cand", 3)
+    st.diff()
+    st.guard()
+    torch.cuda.synchronize()
+    P = oracle.Prepared(w)
+    for side, v in (("ref", 0), ("cand", 3)):
+        want = np.full(w.arena_bytes, 0xA5, dtype=np.uint8)
+        for k, a in enumerate(allocs):
+            want[offsets[k]:offsets[k] + a.total_bytes] = P.fill_alloc(k, v)
+        assert_bytes_equal(st.arena_host(side), want, f"phases {side}")
+    cand, ref = st.arena_host("cand"), st.arena_host("ref")
+    from oracle import diff_workload, guard_workload
+    assert_results_equal(st.seg_results(), diff_workload(w, cand, ref), "phases diff")
+    assert_results_equal(st.guard_results(), guard_workload(w, cand), "phases guards")

@@ -38,8 +38,15 @@ def workload_seed(n: int) -> int:
 
 
 def rate_threshold(rate: float) -> int:
-    """Bernoulli selection threshold T on a 32-bit uniform: selected iff x < T."""
-    return int(round(rate * 2.0 ** 32))
+    """Bernoulli selection threshold T on a 32-bit uniform (selected iff x < T)
+    for a rate 0 <= r <= 1: T = floor(r * 2^32 + 1/2), 2^32 for r = 1 -- the
+    rule the library applies to the rate of its BOUNDARY distribution.  Both
+    the library's binding and the oracle's take a RATE rule's T from here."""
+    if not 0.0 <= rate <= 1.0:
+        raise ValueError(f"rate {rate} outside [0, 1]")
+    if rate == 1.0:
+        return 1 << 32
+    return int(math.floor(rate * 4294967296.0 + 0.5))   # rate * 2^32 is exact; so is + 1/2 below 2^52
 
 
 @dataclass(frozen=True)
