@@ -528,7 +528,7 @@ static int pad_written(const ref_inj* inj, int64_t n_inj, int32_t k, uint32_t va
   return hit;
 }
 
-int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64_t n_inj,
+int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* all_inj, int64_t n_all,
                    uint64_t seed, uint32_t variant, int64_t off, int64_t nbytes, uint8_t* out) {
   const ref_alloc* A = &allocs[k];
   int es = ref_esize(A->dtype);
@@ -537,6 +537,14 @@ int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64
   int64_t D = data_bytes(A);
   int64_t total = A->guard_lo + D + A->guard_hi;
   if (off + nbytes > total) return -1;
+  /* only allocation k's entries, in list order (the others are skipped for
+   * every byte anyway; a workload with an entry per allocation would
+   * otherwise scan them all for every element) */
+  ref_inj* inj = (ref_inj*)malloc(sizeof(ref_inj) * (size_t)(n_all > 0 ? n_all : 1));
+  if (!inj) return -1;
+  int64_t n_inj = 0;
+  for (int64_t t = 0; t < n_all; ++t)
+    if (all_inj[t].alloc == (uint32_t)k) inj[n_inj++] = all_inj[t];
   int64_t cached_e = -1;
   uint64_t cached_bits = 0;
   for (int64_t n = 0; n < nbytes; ++n) {
@@ -567,6 +575,7 @@ int ref_fill_range(const ref_alloc* allocs, int32_t k, const ref_inj* inj, int64
     }
     out[n] = byte;
   }
+  free(inj);
   return 0;
 }
 

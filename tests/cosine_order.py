@@ -59,24 +59,41 @@ def pairwise_tree(x: Sequence[float]) -> float:
     return perfect_tree(x[:h]) + pairwise_tree(x[h:])
 
 
+_TABLES: Dict[str, Tuple[np.ndarray, np.ndarray]] = {}
+
+
 def _values(dtype: str, raw: np.ndarray):
-    cls, val = oracle.decode_n(dtype, raw.astype(np.uint64))
-    return cls == 0, val
+    """(finite mask, exact float64 values) of raw elements: the oracle's decode,
+    tabulated once over every pattern of the 8- and 16-bit types; binary32 by
+    numpy's exact widening."""
+    if dtype == "f32":
+        with np.errstate(invalid="ignore"):      # NaN patterns widen to NaN
+            v = raw.astype(np.uint32).view(np.float32).astype(np.float64)
+        return np.isfinite(v), v
+    if dtype not in _TABLES:
+        n = 1 << (8 * ESIZE[dtype])
+        cls, val = oracle.decode_n(dtype, np.arange(n, dtype=np.uint64))
+        _TABLES[dtype] = (cls == 0, val)
+    ok, val = _TABLES[dtype]
+    idx = raw.astype(np.intp)
+    return ok[idx], val[idx]
 
 
-def rows_block_sums(dtype: str, ra: np.ndarray, rb: np.ndarray) -> np.ndarray:
+def rows_block_sums(dtype: str, ra: np.ndarray, rb: np.ndarray) -> Tuple[np.ndarray, int]:
     """[rows * blocks_per_row, 3] sums (ab, aa, bb), row-major, of rows of equal
-    length given the raw elements of both operands ([rows, length] arrays)."""
+    length given the raw elements of both operands ([rows, length] arrays),
+    and the number of pairs with both values finite."""
     R, n = ra.shape
     per_block = 4096 // ESIZE[dtype]
     if R == 1 and n > _PIECE:                    # one long row: whole blocks at a time
         step = _PIECE // per_block * per_block
-        return np.concatenate([_block_sums(dtype, ra[:, k:k + step], rb[:, k:k + step])
-                               for k in range(0, n, step)])
-    if R > 1 and R * n > _PIECE:
+        parts = [_block_sums(dtype, ra[:, k:k + step], rb[:, k:k + step]) for k in range(0, n, step)]
+    elif R > 1 and R * n > _PIECE:
         step = max(1, _PIECE // max(n, 1))
-        return np.concatenate([_block_sums(dtype, ra[k:k + step], rb[k:k + step]) for k in range(0, R, step)])
-    return _block_sums(dtype, ra, rb)
+        parts = [_block_sums(dtype, ra[k:k + step], rb[k:k + step]) for k in range(0, R, step)]
+    else:
+        parts = [_block_sums(dtype, ra, rb)]
+    return np.concatenate([p[0] for p in parts]), sum(p[1] for p in parts)
 
 
 def _block_sums(dtype: str, ra: np.ndarray, rb: np.ndarray) -> np.ndarray:
@@ -85,23 +102,26 @@ def _block_sums(dtype: str, ra: np.ndarray, rb: np.ndarray) -> np.ndarray:
     R, n = ra.shape
     nb = -(-n // per_block)
     if R == 0 or nb == 0:
-        return np.zeros((0, 3))
+        return np.zeros((0, 3)), 0
     fa, A = _values(dtype, ra)
     fb, B = _values(dtype, rb)
     ok = fa & fb
+    A = np.where(ok, A, 0.0)                     # an excluded or missing product adds +0.0: no change
+    B = np.where(ok, B, 0.0)
     terms = np.zeros((3, R, nb * per_block))
-    terms[0, :, :n] = np.where(ok, A * B, 0.0)   # an excluded or missing product adds +0.0: no change
-    terms[1, :, :n] = np.where(ok, A * A, 0.0)
-    terms[2, :, :n] = np.where(ok, B * B, 0.0)
-    t = terms.reshape(3, R * nb, 4, 64, epc)     # element of a block = ((j * 64 + lane) * epc + e)
+    terms[0, :, :n] = A * B
+    terms[1, :, :n] = A * A
+    terms[2, :, :n] = B * B
+    # element of a block = ((j * 64 + lane) * epc + e): order the terms (j, e, ..., lane)
+    t = np.ascontiguousarray(terms.reshape(3, R * nb, 4, 64, epc).transpose(2, 4, 0, 1, 3))
     lanes = np.zeros((3, R * nb, 64))
     for j in range(4):
         for e in range(epc):
-            lanes = lanes + t[:, :, j, :, e]
+            lanes += t[j, e]
     idx = np.arange(64)
     for m in (32, 16, 8, 4, 2, 1):
         lanes = lanes + lanes[:, :, idx ^ m]
-    return lanes[:, :, 0].T
+    return lanes[:, :, 0].T, int(np.count_nonzero(ok))
 
 
 def _finish(blocks: np.ndarray, pairs: int) -> Dict:
@@ -121,21 +141,17 @@ def _undefined() -> Dict:
     return {"sum_ab": 0.0, "sum_aa": 0.0, "sum_bb": 0.0, "cosine": math.nan, "pairs": 0, "blocks": 0}
 
 
-def _gather(buf: np.ndarray, off: int, es: int, idx: np.ndarray) -> np.ndarray:
-    if idx.size == 0:
-        return np.zeros(0, dtype=np.uint64)
-    pos = off + idx.astype(np.int64) * es
-    b = buf.view(np.uint8)
-    out = np.zeros(idx.shape, dtype=np.uint64)
-    for k in range(es):                          # little endian
-        out |= b[pos + k].astype(np.uint64) << np.uint64(8 * k)
-    return out
-
-
-def _pairs(ra, rb, dtype) -> int:
-    fa, _ = _values(dtype, ra)
-    fb, _ = _values(dtype, rb)
-    return int(np.count_nonzero(fa & fb))
+def _strided(buf: np.ndarray, off: int, es: int, shape: Sequence[int], strides: Sequence[int]) -> np.ndarray:
+    """Raw elements (as uint64) of the view with this shape and these element
+    strides, starting at byte `off` of buf."""
+    b = np.ascontiguousarray(buf).view(np.uint8).reshape(-1)
+    shape = [int(n) for n in shape]
+    if any(n == 0 for n in shape):
+        return np.zeros(shape, dtype=np.uint64)
+    view = np.lib.stride_tricks.as_strided(b[off:], shape=shape + [es], strides=[int(x) * es for x in strides] + [1],
+                                           writeable=False)
+    raw = np.ascontiguousarray(view).view("<u%d" % es)[..., 0]
+    return raw.astype(np.uint64)
 
 
 def cosine_2d(dtype: str, rows: int, cols: int, sa: int, sb: int, a: np.ndarray, b: np.ndarray,
@@ -147,13 +163,12 @@ def cosine_2d(dtype: str, rows: int, cols: int, sa: int, sb: int, a: np.ndarray,
     if rows <= 0 or cols <= 0:
         return _finish(np.zeros((0, 3)), 0)
     if rows == 1 or (sa == cols and sb == cols):
-        ia = ib = np.arange(rows * cols)[None, :]
+        ra = _strided(a, a_off, es, [1, rows * cols], [0, 1])
+        rb = _strided(b, b_off, es, [1, rows * cols], [0, 1])
     else:
-        c = np.arange(cols)[None, :]
-        r = np.arange(rows)[:, None]
-        ia, ib = r * sa + c, r * sb + c
-    ra, rb = _gather(a, a_off, es, ia), _gather(b, b_off, es, ib)
-    return _finish(rows_block_sums(dtype, ra, rb), _pairs(ra, rb, dtype))
+        ra = _strided(a, a_off, es, [rows, cols], [sa, 1])
+        rb = _strided(b, b_off, es, [rows, cols], [sb, 1])
+    return _finish(*rows_block_sums(dtype, ra, rb))
 
 
 def walk(shape: Sequence[int], sa: Sequence[int], sb: Sequence[int]) -> List[Tuple[int, int, int]]:
@@ -187,17 +202,11 @@ def cosine_nd(dtype: str, parts: Sequence, a: np.ndarray, b: np.ndarray) -> Dict
     for shape, sa, sb, a_off, b_off in parts:
         if any(n == 0 for n in shape):
             continue
-        w = walk(shape, sa, sb)
-        n_in, in_a, in_b = w[-1]
-        oa = np.zeros(1, dtype=np.int64)
-        ob = np.zeros(1, dtype=np.int64)
-        for n, x, y in w[:-1]:                   # rows: outer dimensions, last fastest
-            k = np.arange(n, dtype=np.int64)
-            oa = (oa[:, None] + k[None, :] * x).ravel()
-            ob = (ob[:, None] + k[None, :] * y).ravel()
-        j = np.arange(n_in, dtype=np.int64)[None, :]
-        ra = _gather(a, a_off, es, oa[:, None] + j * in_a)
-        rb = _gather(b, b_off, es, ob[:, None] + j * in_b)
-        blocks.append(rows_block_sums(dtype, ra, rb))
-        pairs += _pairs(ra, rb, dtype)
+        w = walk(shape, sa, sb)                  # rows: the outer dimensions, last fastest
+        dims = [d[0] for d in w]
+        ra = _strided(a, a_off, es, dims, [d[1] for d in w]).reshape(-1, dims[-1])
+        rb = _strided(b, b_off, es, dims, [d[2] for d in w]).reshape(-1, dims[-1])
+        sums, p = rows_block_sums(dtype, ra, rb)
+        blocks.append(sums)
+        pairs += p
     return _finish(np.concatenate(blocks) if blocks else np.zeros((0, 3)), pairs)

@@ -52,40 +52,6 @@ def assert_fill_equal(w, gpu_arena: np.ndarray, ora_arena: np.ndarray, what=""):
                            f"{what} alloc {k} ({a.dtype} {a.rows}x{a.cols}/{a.stride})")
 
 
-def fill_windows(w, k, rng, n_random=16, width=4096):
-    """Byte windows of allocation k worth checking: both ends, the guards,
-    windows around every point injection, and random windows."""
-    a = w.allocs[k]
-    tot = a.total_bytes
-    wins = [(0, min(tot, width)), (max(0, tot - width), min(tot, width))]
-    if a.guard_lo:
-        wins.append((0, a.guard_lo))
-    if a.guard_hi:
-        wins.append((a.guard_lo + a.data_bytes, a.guard_hi))
-    for j in w.injections:
-        if j.alloc != k or j.rate is not None or j.kind.startswith("guard"):
-            continue
-        r, c = divmod(j.index, a.cols)
-        off = a.guard_lo + (r * a.stride + c) * a.esize
-        s = max(0, off - 64)
-        wins.append((s, min(128, tot - s)))
-    for _ in range(n_random):
-        if tot > width:
-            s = int(rng.integers(0, tot - width))
-            wins.append((s, width))
-    return [(s, n) for s, n in wins if n > 0]
-
-
-def check_fill_sampled(w, st, variant_of_side, rng, n_random=16, width=4096):
-    P = oracle.Prepared(w)
-    for side, variant in variant_of_side.items():
-        for k in range(len(w.allocs)):
-            for s, n in fill_windows(w, k, rng, n_random, width):
-                got = st.alloc_bytes(side, k, s, n)
-                want = P.fill_range(k, variant, s, n)
-                assert_bytes_equal(got, want, f"{side} alloc {k} bytes [{s}, {s + n})")
-
-
 # ------------------------------------------------------------ the cosine term
 U = 2.0 ** -53
 

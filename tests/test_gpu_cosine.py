@@ -31,6 +31,7 @@ def test_cosine_reduced_workloads(name):
     assert_cosine(got, *cosine_workload_expected(w, cand, ref), f"{name} cosine")
 
 
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("name", ["single_fp32", "padded_bf16", "decode_state", "int_lowp"])
 def test_cosine_full_size(name):
     w = workloads.ALL[name]()
@@ -126,6 +127,7 @@ def test_cosine_every_fp8_and_f16_value():
         _check(got, specs, a_h, b_h, f"{dtype} every value")
 
 
+@pytest.mark.timeout(300)
 def test_cosine_tree_levels_with_leftovers():
     """Segments whose block counts leave entries at every level of the block
     tree: 65536 + 5 * 256 + 3 blocks (one level-2 group, five level-1

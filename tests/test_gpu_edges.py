@@ -328,14 +328,14 @@ def test_fill_element_aligned_bases():
         ghi = 3 * (k % 4)
         dist, kw = dists[dt]
         allocs.append(Alloc(k, dt, rows, cols, stride, glo, ghi, dist, **kw))
-        offsets.append(1024 * k + phase)
+        offsets.append(2048 * k + phase)
         inj.append(Injection(k, "flip_bit", arg=-1, rate=0.3))
         if ghi:
             inj.append(Injection(k, "guard_write_hi", arg=1, index=ghi - 1))
     compares = [Compare(k, "tolerance" if a.dtype in ("f32", "bf16", "f16", "fp8e4m3") else "bitwise",
                         "equal", 1e-3, 1e-3) for k, a in enumerate(allocs)]
-    w = Workload("phases", "", 0x5EED, allocs, inj, compares, offsets=offsets, arena_bytes=1024 * len(specs))
-    assert all(offsets[k] + a.total_bytes <= 1024 * (k + 1) for k, a in enumerate(allocs))
+    w = Workload("phases", "", 0x5EED, allocs, inj, compares, offsets=offsets, arena_bytes=2048 * len(specs))
+    assert all(offsets[k] + a.total_bytes <= 2048 * (k + 1) for k, a in enumerate(allocs))
     log(f"[phases] {len(allocs)} allocations")
     st = DeviceState(w)
     st.ref.fill_(0xA5)
