@@ -63,7 +63,8 @@ enum {
   ASMEVO_E_INVALID = -1,      /* malformed descriptor or argument */
   ASMEVO_E_UNSUPPORTED = -2,  /* valid but not supported (e.g. +-Inf in fp8 e4m3) */
   ASMEVO_E_WORKSPACE = -3,    /* workspace missing or smaller than required */
-  ASMEVO_E_HIP = -4           /* a HIP runtime call failed */
+  ASMEVO_E_HIP = -4,          /* a HIP runtime call failed */
+  ASMEVO_E_CAPACITY = -5      /* more descriptors than a fixed-size call holds */
 };
 
 /* element types */
@@ -251,6 +252,24 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
                                       asmevo_segment_result* results,
                                       void* workspace, size_t ws_bytes, void* stream,
                                       int32_t workgroups);
+
+/*
+ * asmevo_diff_segments_noalloc -- asmevo_diff_segments for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): no workspace argument; the
+ * descriptor table goes to a static device array of the library that holds
+ * ASMEVO_NOALLOC_MAX_SEGMENTS descriptors (512 KiB; each GPU the library runs
+ * on keeps its own copy until the process ends).  The call allocates nothing
+ * (no hipMalloc, no hipFree, no allocating library routine).  Results are
+ * identical to asmevo_diff_segments'.  Every call on one GPU shares that
+ * GPU's array: calls whose work overlaps on one GPU (other streams, other
+ * threads before their stream has drained) race and give undefined results;
+ * calls in one stream are ordered.  Errors as for asmevo_diff_segments, and
+ * ASMEVO_E_CAPACITY for n > ASMEVO_NOALLOC_MAX_SEGMENTS.
+ */
+#define ASMEVO_NOALLOC_MAX_SEGMENTS 4096
+asmevo_status asmevo_diff_segments_noalloc(const asmevo_segment* segs, int32_t n,
+                                           asmevo_segment_result* results, void* stream);
 
 /*
  * One N-dimensional compared buffer pair (section 3.4: captured dispatch

@@ -18,7 +18,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("ASMEVO_LIBRARY") or os.path.join(PKG, "libasmevo.so")
 
 # codes of include/asmevo.h
-OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, -1, -2, -3, -4
+OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP, E_CAPACITY = 0, -1, -2, -3, -4, -5
+NOALLOC_MAX_SEGMENTS = 4096
 F32, BF16, F16, FP8_E4M3, I32, I64, U8 = 1, 2, 3, 4, 5, 6, 7
 BITWISE, TOLERANCE = 0, 1
 NAN_EQUAL, NAN_STRICT = 0, 1
@@ -125,7 +126,8 @@ EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments
             "asmevo_abi_version", "asmevo_last_hip_error", "asmevo_diff_segments_nd",
             "asmevo_diff_nd_workspace_bytes", "asmevo_kernel_load", "asmevo_kernel_unload",
             "asmevo_kernel_launch", "asmevo_kernel_time", "asmevo_va_granularity", "asmevo_va_alloc",
-            "asmevo_va_free", "asmevo_diff_cosine_nd", "asmevo_diff_cosine_nd_workspace_bytes"]
+            "asmevo_va_free", "asmevo_diff_cosine_nd", "asmevo_diff_cosine_nd_workspace_bytes",
+            "asmevo_diff_segments_noalloc"]
 
 
 class AsmevoError(RuntimeError):
@@ -159,6 +161,8 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_diff_segments_ex.argtypes = [P(Segment), ctypes.c_int32, vp, vp, ctypes.c_size_t, vp,
                                               ctypes.c_int32]
         L.asmevo_diff_segments_ex.restype = ctypes.c_int32
+        L.asmevo_diff_segments_noalloc.argtypes = [P(Segment), ctypes.c_int32, vp, vp]
+        L.asmevo_diff_segments_noalloc.restype = ctypes.c_int32
         L.asmevo_diff_cosine.argtypes = [P(Segment), ctypes.c_int32, vp, vp, vp, ctypes.c_size_t, vp]
         L.asmevo_diff_cosine.restype = ctypes.c_int32
         L.asmevo_diff_segments_nd.argtypes = [P(SegmentND), ctypes.c_int32, vp, ctypes.c_int32, vp,
@@ -261,6 +265,13 @@ def diff_segments(segments: Sequence[Segment], results_ptr: int, workspace_ptr: 
     _check(_lib().asmevo_diff_segments_ex(s, len(segments), results_ptr, workspace_ptr,
                                           workspace_size, _stream_handle(stream), workgroups),
            "asmevo_diff_segments")
+
+
+def diff_segments_noalloc(segments: Sequence[Segment], results_ptr: int, stream=None) -> None:
+    """asmevo_diff_segments without a workspace (its table in the library's static device array)."""
+    s = _array(Segment, segments)
+    _check(_lib().asmevo_diff_segments_noalloc(s, len(segments), results_ptr, _stream_handle(stream)),
+           "asmevo_diff_segments_noalloc")
 
 
 def diff_nd_workspace_bytes(n: int) -> int:

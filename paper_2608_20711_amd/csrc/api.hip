@@ -104,6 +104,7 @@ const char* asmevo_status_string(asmevo_status s) {
     case ASMEVO_E_UNSUPPORTED: return "unsupported";
     case ASMEVO_E_WORKSPACE: return "workspace missing or too small";
     case ASMEVO_E_HIP: return "HIP runtime error";
+    case ASMEVO_E_CAPACITY: return "more descriptors than the static scratch array holds";
     default: return "unknown status";
   }
 }
@@ -638,6 +639,64 @@ asmevo_status asmevo_diff_segments(const asmevo_segment* segs, int32_t n,
   return asmevo_diff_segments_ex(segs, n, results, workspace, ws_bytes, stream, 0);
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The diff for callers that cannot allocate: its descriptor table, the only
+// scratch the plain diff uses, lives in a static device array instead of a
+// workspace.  Each device holds its own copy of `scratch` until the process
+// ends; host code never names the array itself (in host code it is a
+// stand-in, not a device address) but the address that hipGetSymbolAddress
+// gives for the current device, looked up on the first call on that device.
+// The host-side table is planned into a static array too, under a mutex.
+namespace {
+
+__attribute__((used)) static __device__ __align__(256) DiffSeg scratch[ASMEVO_NOALLOC_MAX_SEGMENTS];
+
+constexpr int kMaxDevices = 64;
+std::atomic<uint64_t> g_scratch_addr[kMaxDevices];   // 0 until looked up
+std::mutex g_noalloc_mutex;                          // guards g_noalloc_host
+DiffSeg g_noalloc_host[ASMEVO_NOALLOC_MAX_SEGMENTS];
+
+asmevo_status scratch_of_current_device(DiffSeg** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return ASMEVO_E_UNSUPPORTED;
+  uint64_t a = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (a == 0) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return ASMEVO_E_HIP;
+    a = reinterpret_cast<uint64_t>(p);
+    g_scratch_addr[dev].store(a, std::memory_order_release);
+  }
+  *out = reinterpret_cast<DiffSeg*>(a);
+  return ASMEVO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+asmevo_status asmevo_diff_segments_noalloc(const asmevo_segment* segs, int32_t n,
+                                           asmevo_segment_result* results, void* stream) {
+  if (n < 0 || (n > 0 && (!segs || !results))) return ASMEVO_E_INVALID;
+  if (n > ASMEVO_NOALLOC_MAX_SEGMENTS) return ASMEVO_E_CAPACITY;
+  if (n == 0) return ASMEVO_OK;
+  std::lock_guard<std::mutex> lock(g_noalloc_mutex);
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff(segs, n, false, g_noalloc_host, tiles);
+  if (st != ASMEVO_OK) return st;
+  DiffSeg* table = nullptr;
+  st = scratch_of_current_device(&table);
+  if (st != ASMEVO_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // pageable source: HIP has read it when the call returns, so the host
+  // table may be planned again by the next call
+  HIP_TRY(hipMemcpyAsync(table, g_noalloc_host, (size_t)n * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_diff(table, n, tiles, results, device_cus(), s));
+  return ASMEVO_OK;
+}
 
 size_t asmevo_diff_nd_workspace_bytes(int32_t n) {
   const size_t m = n > 0 ? (size_t)n : 0;

@@ -287,3 +287,18 @@ def test_diff_nd_ndim_and_workspace():
         lib.diff_segments_nd([_seg_nd()], 0, 1, 0x50000, need, stream=0)
     assert e.value.status == lib.E_INVALID
 
+
+def test_noalloc_diff_argument_errors():
+    """The allocation-free diff validates before touching the GPU: more
+    segments than its static table holds, a null result pointer, a negative
+    count and malformed segments are refused."""
+    L = lib.lib()
+    n = lib.NOALLOC_MAX_SEGMENTS + 1
+    arr = (lib.Segment * n)(*[_seg()] * n)
+    assert L.asmevo_diff_segments_noalloc(arr, n, 0x1000, None) == lib.E_CAPACITY
+    assert L.asmevo_diff_segments_noalloc(arr, 1, None, None) == lib.E_INVALID
+    assert L.asmevo_diff_segments_noalloc(arr, -1, 0x1000, None) == lib.E_INVALID
+    bad = (lib.Segment * 1)(_seg(stride_a=1, cols=5))
+    assert L.asmevo_diff_segments_noalloc(bad, 1, 0x1000, None) == lib.E_INVALID
+    assert L.asmevo_diff_segments_noalloc(arr, 0, 0x1000, None) == lib.OK
+    assert b"static" in L.asmevo_status_string(lib.E_CAPACITY)
