@@ -84,6 +84,16 @@ int device_cus() {
   return cus;
 }
 
+// Workgroups of the plain diff: persistent, one (4 waves) per CU when the
+// state is large -- on the 64 GiB sweep that streams 1.5-2 % faster than the
+// full resident set, whose more concurrent read streams cost DRAM locality --
+// and two per CU below 4 GiB of operands, where the second wave per SIMD
+// hides the slow path of states with many differences (decode state +4 %).
+int diff_workgroups(uint64_t tiles) {
+  const uint64_t operand_bytes = tiles * (uint64_t)kTileChunks * kChunk * 2;
+  return device_cus() * (operand_bytes < (4ull << 30) ? 2 : 1);
+}
+
 template <typename T>
 void put(std::vector<uint8_t>& buf, size_t off, const std::vector<T>& v) {
   if (!v.empty()) std::memcpy(buf.data() + off, v.data(), v.size() * sizeof(T));
@@ -625,10 +635,7 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
   int wg = workgroups;
-  // One workgroup (4 waves) per CU, persistent: on the 64 GiB sweep it streams
-  // ~1 % faster than a full resident set (4 per CU), whose 4x more concurrent
-  // read streams cost DRAM locality; each lane keeps 8 loads in flight.
-  if (wg == 0) wg = device_cus();
+  if (wg == 0) wg = diff_workgroups(tiles);
   HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(workspace), n, tiles, results, wg, s));
   return ASMEVO_OK;
 }
@@ -694,7 +701,7 @@ asmevo_status asmevo_diff_segments_noalloc(const asmevo_segment* segs, int32_t n
   // pageable source: HIP has read it when the call returns, so the host
   // table may be planned again by the next call
   HIP_TRY(hipMemcpyAsync(table, g_noalloc_host, (size_t)n * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_diff(table, n, tiles, results, device_cus(), s));
+  HIP_TRY(launch_diff(table, n, tiles, results, diff_workgroups(tiles), s));
   return ASMEVO_OK;
 }
 

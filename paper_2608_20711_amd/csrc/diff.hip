@@ -222,6 +222,229 @@ __device__ __forceinline__ void chunk(const u32x4& va, const u32x4& vb, uint64_t
   }
 }
 
+// ------------------------------------------------------- slow path of a tile
+// A tile whose chunk pairs hold differences (or, under the strict NaN
+// policy, any tile) runs the per-pair rule for every element its need masks
+// mark.  Left to each lane, the rule runs as often as the busiest lane has
+// marked elements, with the other lanes idle: with 1 % of the elements
+// differing (a GEMM output's last-bit flips) nearly every tile takes ~1.1
+// rounds of the ~110-instruction rule per chunk row, four rows a tile.  So
+// the marked elements of the whole tile are first gathered into the wave's
+// slot of LDS (each lane appends its own, at an offset from a wave-wide
+// prefix sum of the counts), and the rule then runs once per 64 of them, one
+// element per lane.  A tile with more than kSlowCap marked elements (dense
+// differences, where every lane is busy anyway) keeps the per-lane loop.
+// BITWISE segments need no rule: counts and first indices come from the
+// masks directly.
+constexpr uint32_t kSlowCap = 256;
+struct SlowEntry {       // 16 bytes
+  uint32_t ra, rb;       // raw element bits (at most 4 bytes: the rule runs on float types only)
+  uint64_t idx;          // logical index, or walk position of a reordered N-D segment
+};
+
+__device__ __forceinline__ uint32_t valid_mask(uint32_t nvalid) {
+  return nvalid >= 32u ? ~0u : ((1u << nvalid) - 1u);
+}
+
+// The wave's marked elements of U chunk pairs: chunk j holds elements
+// i0[j] + e, e < nv[j].  The whole wave must be active (the prefix sum and
+// the total are wave-wide); callers branch on wave-uniform conditions only.  (The cosine
+// variants keep the per-lane loop: the gathering would exceed their
+// register budget.)
+template <int DT, bool ND, bool COMPACT, int U>
+__device__ __forceinline__ void tile_slow(const u32x4 (&va)[U], const u32x4 (&vb)[U], const uint64_t (&i0)[U],
+                                          const uint32_t (&nv)[U], uint32_t lane, bool tol_mode, bool strict,
+                                          double atol, double rtol, Acc& acc, const NdExt* X, bool permuted,
+                                          SlowEntry* slot) {
+  if constexpr (!COMPACT) {
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      chunk<DT, ND>(va[j], vb[j], i0[j], nv[j], tol_mode, strict, atol, rtol, acc, X, permuted);
+    return;
+  }
+  uint32_t m[U];
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    const u32x4 x = va[j] ^ vb[j];
+    m[j] = (((x.x | x.y | x.z | x.w) == 0u) && !strict) ? 0u : need_mask<DT>(va[j], vb[j], strict);
+    m[j] &= valid_mask(nv[j]);
+    cnt += (uint32_t)__builtin_popcount(m[j]);
+  }
+  if (!Et<DT>::fp || !tol_mode) {
+    // bits differ: that is the whole verdict (need masks mark exactly the
+    // differing elements when the policy is not strict)
+    acc.bw += cnt;
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      if (m[j] == 0u) continue;
+      uint64_t i = i0[j] + (uint64_t)__builtin_ctz(m[j]);
+      if constexpr (ND) {
+        if (permuted) {                        // the lowest logical index need not be the first in walk order
+          uint32_t mm = m[j];
+          i = ~0ull;
+          while (mm) {
+            const uint64_t q = nd_logical(X, i0[j] + (uint64_t)__builtin_ctz(mm));
+            mm &= mm - 1u;
+            i = q < i ? q : i;
+          }
+        }
+      }
+      acc.first_bw = i < acc.first_bw ? i : acc.first_bw;
+    }
+    return;
+  }
+  // exclusive prefix sum of the lanes' counts, and the wave's total
+  uint32_t inc = cnt;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const uint32_t o = (uint32_t)__shfl_up((int)inc, (unsigned)d, kWave);
+    inc += lane >= (uint32_t)d ? o : 0u;
+  }
+  const uint32_t total = (uint32_t)__shfl((int)inc, kWave - 1, kWave);
+  if (total > kSlowCap) {                      // dense: every lane has work of its own
+#pragma unroll
+    for (int j = 0; j < U; ++j)
+      chunk<DT, ND>(va[j], vb[j], i0[j], nv[j], tol_mode, strict, atol, rtol, acc, X, permuted);
+    return;
+  }
+  uint32_t off = inc - cnt;
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    uint32_t mm = m[j];
+    while (mm) {
+      const uint32_t e = (uint32_t)__builtin_ctz(mm);
+      mm &= mm - 1u;
+      SlowEntry E;
+      E.ra = (uint32_t)elem_dyn<DT>(va[j], e);
+      E.rb = (uint32_t)elem_dyn<DT>(vb[j], e);
+      E.idx = i0[j] + (uint64_t)e;
+      slot[off++] = E;
+    }
+  }
+  // the entries of every lane are in LDS before any lane reads them
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  for (uint32_t k = lane; k < total; k += kWave) {
+    const SlowEntry E = slot[k];
+    uint64_t i = E.idx;
+    if constexpr (ND) {
+      if (permuted) i = nd_logical(X, i);
+    }
+    pair_slow<DT>(E.ra, E.rb, i, true, strict, atol, rtol, acc);
+  }
+  // every lane has read its entries before the slot is written again
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// A whole tile's slow path is deferred: every lane copies its four chunk
+// pairs to the wave's slot of LDS (fixed places, no branches: 8 KiB per
+// tile), a ballot per chunk row marks the chunk pairs that need the rule
+// (bits differ, or under the strict policy b holds a NaN), and the rule runs
+// on the marked ones, one per lane, after the next tile's loads have been
+// issued, so that it overlaps their latency instead of adding to it.
+constexpr uint32_t kSlotBytes = 8192;   // per wave: a tile's chunk pairs
+static_assert(2u * kTileChunks * kChunk <= kSlotBytes, "a tile's chunk pairs fit the slot");
+static_assert(kSlowCap * sizeof(SlowEntry) <= kSlotBytes, "element gathering fits the slot");
+
+// Does any element of the chunk hold a NaN?
+template <int DT>
+__device__ __forceinline__ bool any_nan(const u32x4& v) {
+  uint32_t hit = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t w = v[k];
+    if constexpr (DT == ASMEVO_F32) hit |= (w & 0x7FFFFFFFu) > 0x7F800000u ? 1u : 0u;
+    else if constexpr (DT == ASMEVO_BF16) hit |= ((w & 0x7FFF7FFFu) + 0x007F007Fu) & 0x80008000u;
+    else if constexpr (DT == ASMEVO_F16) hit |= ((w & 0x7FFF7FFFu) + 0x03FF03FFu) & 0x80008000u;
+    else if constexpr (DT == ASMEVO_FP8_E4M3) hit |= ((w & 0x7F7F7F7Fu) + 0x01010101u) & 0x80808080u;
+  }
+  return hit != 0u;
+}
+
+// The marked chunk pairs of a staged tile: ballot masks per chunk row.
+template <int U>
+struct Staged {
+  uint64_t mask[U];
+  uint32_t count;        // marked chunk pairs (wave-uniform)
+  uint64_t ibase, k0;    // the tile's first logical index and first chunk
+};
+
+// Copies the chunk pairs of a whole tile to the slot (a at [0, 256), b at
+// [256, 512) in 16-byte units, chunk j * 64 + lane) and marks those that
+// need the rule.  The whole wave must be active.
+template <int DT, int U>
+__device__ __forceinline__ void stage_tile(const u32x4 (&va)[U], const u32x4 (&vb)[U], uint32_t lane, bool strict,
+                                           uint64_t ibase, uint64_t k0, u32x4* slot, Staged<U>& st) {
+  st.count = 0;
+  st.ibase = ibase;
+  st.k0 = k0;
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    slot[j * kWave + lane] = va[j];
+    slot[kTileChunks + j * kWave + lane] = vb[j];
+    const u32x4 x = va[j] ^ vb[j];
+    bool need = (x.x | x.y | x.z | x.w) != 0u;
+    if (strict) need = need || any_nan<DT>(vb[j]);
+    st.mask[j] = __ballot(need);
+    st.count += (uint32_t)__builtin_popcountll(st.mask[j]);
+  }
+}
+
+// Position of the r-th set bit (r counted from 0) of m, which has more than
+// r set bits: a binary search over bit counts, without branches.
+__device__ __forceinline__ uint32_t nth_set_bit(uint64_t m, uint32_t r) {
+  uint32_t pos = 0;
+  uint32_t c = (uint32_t)__builtin_popcount((uint32_t)m);
+  const bool hi = r >= c;
+  r -= hi ? c : 0u;
+  uint32_t w = hi ? (uint32_t)(m >> 32) : (uint32_t)m;
+  pos += hi ? 32u : 0u;
+#pragma unroll
+  for (int half = 16; half >= 1; half >>= 1) {
+    c = (uint32_t)__builtin_popcount(w & ((1u << half) - 1u));
+    const bool up = r >= c;
+    r -= up ? c : 0u;
+    w = up ? (w >> half) : w;
+    pos += up ? (uint32_t)half : 0u;
+  }
+  return pos;
+}
+
+// The rule on the marked chunk pairs of a staged tile, one per lane.
+template <int DT, bool ND, int U>
+__device__ __forceinline__ void run_staged(const u32x4* slot, const Staged<U>& st, uint32_t lane, bool strict,
+                                           double atol, double rtol, Acc& acc, const NdExt* X, bool permuted) {
+  constexpr int epc = 16 / Et<DT>::es;
+  // the stores of every lane are in LDS before any lane reads them
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  for (uint32_t k = lane; k < st.count; k += kWave) {
+    uint32_t r = k, j = 0;
+#pragma unroll
+    for (int q = 0; q + 1 < U; ++q) {    // the chunk row holding the k-th marked pair
+      const uint32_t c = (uint32_t)__builtin_popcountll(st.mask[q]);
+      const bool next = j == (uint32_t)q && r >= c;
+      r -= next ? c : 0u;
+      j += next ? 1u : 0u;
+    }
+    uint64_t m = st.mask[0];
+#pragma unroll
+    for (int q = 1; q < U; ++q) m = j == (uint32_t)q ? st.mask[q] : m;
+    const uint32_t pos = j * kWave + nth_set_bit(m, r);
+    chunk<DT, ND>(slot[pos], slot[kTileChunks + pos], st.ibase + (st.k0 + pos) * epc, epc, true, strict, atol,
+                  rtol, acc, X, permuted);
+  }
+  // every lane has read before the slot is written again
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Loads the valid elements of a chunk one by one (misaligned operands or a
 // partial chunk at the end of a row); invalid bytes read as zero on both sides.
 template <int DT>
@@ -614,12 +837,16 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
 template <int DT, bool COS, bool ND>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                            uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
-                                           double* partials,
-                                           uint32_t& nonfinite) {
+                                           double* partials, uint32_t& nonfinite, uint8_t* slot_bytes) {
   constexpr int es = Et<DT>::es;
   constexpr int epc = 16 / es;
   constexpr int U = kDiffUnroll;
   constexpr bool kCos = COS && Et<DT>::fp;
+  // whole tiles defer their slow path in the plain 2-D diff only (the N-D
+  // variant would exceed its register budget: 128 for 4 waves per SIMD)
+  constexpr bool kDefer = !COS && !ND;
+  SlowEntry* slot = reinterpret_cast<SlowEntry*>(slot_bytes);
+  u32x4* stage = reinterpret_cast<u32x4*>(slot_bytes);
   const bool tol_mode = S.mode == ASMEVO_TOLERANCE;
   const bool strict = (S.flags & kSegStrict) != 0;
   const bool vec = (S.flags & kSegVec) != 0;
@@ -684,9 +911,10 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           i0[j] = ibase0 + r * S.cols + c * epc;
         }
       }
+      uint32_t nv[U];
 #pragma unroll
-      for (int j = 0; j < U; ++j)
-        chunk<DT, ND>(va[j], vb[j], i0[j], nb[j] / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
+      for (int j = 0; j < U; ++j) nv[j] = nb[j] / es;
+      tile_slow<DT, ND, !COS, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X, permuted, slot);
     }
     return;
   }
@@ -765,11 +993,82 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       // runs straight through to the next tile's loads with one taken branch;
       // with the slow path inline and jumped over, the sweep measured 1-2 %
       // slower)
-      if (__builtin_expect(((x.x | x.y | x.z | x.w) != 0u) || strict, 0)) {
+      // (the gathering slow path needs the whole wave: the branch is taken by
+      // every lane when any lane's chunks differ)
+      if (__builtin_expect(__ballot((x.x | x.y | x.z | x.w) != 0u) != 0ull || strict, 0)) {
+        if constexpr (COS) {
 #pragma unroll
-        for (int j = 0; j < U; ++j)
-          chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, nv[j], tol_mode,
-                        strict, S.atol, S.rtol, acc, X, permuted);
+          for (int j = 0; j < U; ++j)
+            chunk<DT, ND>(va[j], vb[j], ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc, nv[j], tol_mode,
+                          strict, S.atol, S.rtol, acc, X, permuted);
+        } else if constexpr (!kDefer) {
+          uint64_t i0[U];
+#pragma unroll
+          for (int j = 0; j < U; ++j) i0[j] = ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc;
+          tile_slow<DT, ND, true, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X, permuted,
+                                     slot);
+        } else {
+          // Slow mode: this tile and the whole tiles after it that need the
+          // rule too, each tile's rule run from LDS while the next tile's
+          // loads are in flight; back to the loop above after the first tile
+          // that needs nothing, or before a tile that is not whole.  (The
+          // loop above is left as it was: checking for staged work there
+          // cost the difference-free sweep 0.6 %.)
+          uint64_t i0[U];
+          uint64_t cur = tile;
+          uint64_t ib = ibase, kc = k0;
+          uint64_t rc = r, ktc = kt;     // row and tile-in-row of `cur`
+          Staged<U> st;
+          bool pending = false;
+          for (;;) {
+            if (Et<DT>::fp && tol_mode) {
+              stage_tile<DT, U>(va, vb, lane, strict, ib, kc, stage, st);
+              pending = st.count != 0;
+            } else {                     // bitwise verdicts: cheap, now
+#pragma unroll
+              for (int j = 0; j < U; ++j) i0[j] = ib + (kc + (uint64_t)(j * kWave) + lane) * epc;
+              tile_slow<DT, ND, true, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X,
+                                         permuted, slot);
+            }
+            const uint64_t nxt = cur + step;
+            if (nxt >= t_end) break;
+            uint64_t r2 = 0, kt2 = nxt;
+            if (S.rows > 1) {
+              if (step == 1) {           // the next tile of the row, or the first of the next row
+                const bool wrap = ktc + 1 == tpr;
+                r2 = wrap ? rc + 1 : rc;
+                kt2 = wrap ? 0 : ktc + 1;
+              } else {
+                r2 = (uint32_t)nxt / (uint32_t)tpr;
+                kt2 = nxt - r2 * tpr;
+              }
+            }
+            const uint64_t k2 = kt2 * (uint64_t)kTileChunks;
+            if (k2 + kTileChunks > S.full_chunks) break;      // not whole: the loop above takes it
+            const uint8_t* qa = a0 + r2 * S.a_pitch + (k2 + lane) * kChunk;
+            const uint8_t* qb = b0 + r2 * S.b_pitch + (k2 + lane) * kChunk;
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+              va[j] = ld_nt(qa + j * kWave * kChunk);
+              vb[j] = ld_nt(qb + j * kWave * kChunk);
+            }
+            if (pending) {               // overlaps the loads just issued
+              run_staged<DT, ND, U>(stage, st, lane, strict, S.atol, S.rtol, acc, X, permuted);
+              pending = false;
+            }
+            cur = nxt;
+            ib = ibase0 + r2 * S.cols;
+            kc = k2;
+            rc = r2;
+            ktc = kt2;
+            u32x4 y = va[0] ^ vb[0];
+#pragma unroll
+            for (int j = 1; j < U; ++j) y |= va[j] ^ vb[j];
+            if (!(__ballot((y.x | y.y | y.z | y.w) != 0u) != 0ull || strict)) break;   // a clean tile: done
+          }
+          if (pending) run_staged<DT, ND, U>(stage, st, lane, strict, S.atol, S.rtol, acc, X, permuted);
+          tile = cur;                    // the loop's step moves past it
+        }
       }
       if constexpr (kCos) {
 #pragma unroll
@@ -809,12 +1108,14 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           else load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
         }
       }
+      uint64_t i0[U];
+      uint32_t nv[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
-        const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
-        chunk<DT, ND>(va[j], vb[j], ibase + c * epc, nb[j] / es, tol_mode, strict, S.atol, S.rtol, acc, X,
-                      permuted);
+        i0[j] = ibase + (k0 + (uint64_t)(j * kWave) + lane) * epc;
+        nv[j] = nb[j] / es;
       }
+      tile_slow<DT, ND, !COS, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X, permuted, slot);
       continue;
     }
 #pragma unroll 1
@@ -918,7 +1219,8 @@ __global__ void diff_init_kernel(asmevo_segment_result* results, int n,
 
 template <bool COS, bool ND>
 __global__ __launch_bounds__(kDiffBlock)
-__attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU : ASMEVO_DIFF_WAVES_PER_EU)))
+__attribute__((amdgpu_waves_per_eu(COS ? ASMEVO_COS_WAVES_PER_EU
+                                        : (ND ? ASMEVO_DIFF_ND_WAVES_PER_EU : ASMEVO_DIFF_WAVES_PER_EU))))
 void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
                  uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                  unsigned long long* nonfinite_pairs) {
@@ -938,6 +1240,9 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
   const uint64_t group = wave / kStep;
   const uint64_t per_group = (total_tiles + ngroups - 1) / ngroups;
   const uint64_t block = kDeal < per_group ? kDeal : per_group;
+  // a slot of LDS per wave for the slow path (the cosine variants use none)
+  __shared__ __align__(16) uint8_t slow[COS ? 16 : (kDiffBlock / kWave) * kSlotBytes];
+  uint8_t* slot = slow + (COS ? 0 : (threadIdx.x / kWave) * kSlotBytes);
   int s = -1;
   Acc acc;
   acc_reset(acc);
@@ -970,15 +1275,15 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
       const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
       const NdExt* X = (ND && S.nd_ext != ~0ull) ? ext + S.nd_ext : nullptr;
       switch (S.dtype) {
-        case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_F32: diff_range<ASMEVO_F32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
+        case ASMEVO_BF16: diff_range<ASMEVO_BF16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
+        case ASMEVO_F16: diff_range<ASMEVO_F16, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
         case ASMEVO_FP8_E4M3:
-          diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
+          diff_range<ASMEVO_FP8_E4M3, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
           break;
-        case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_I32: diff_range<ASMEVO_I32, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
+        case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
+        default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
       }
       flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
       t += (t_end - t + kStep - 1) / kStep * kStep;   // this wave's first tile at or after t_end

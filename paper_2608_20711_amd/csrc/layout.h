@@ -13,8 +13,11 @@ constexpr int kChunk = 16;         // bytes per lane per load (dwordx4)
 #define ASMEVO_DIFF_UNROLL 4
 #endif
 constexpr int kDiffUnroll = ASMEVO_DIFF_UNROLL;      // chunks per lane per tile
-#ifndef ASMEVO_DIFF_WAVES_PER_EU                     // occupancy target of the diff kernel
-#define ASMEVO_DIFF_WAVES_PER_EU 4
+#ifndef ASMEVO_DIFF_WAVES_PER_EU                     // occupancy target of the plain 2-D diff kernel
+#define ASMEVO_DIFF_WAVES_PER_EU 2                   // (it runs 1-2 waves per SIMD: the register budget
+#endif                                               // goes to the deferred slow path)
+#ifndef ASMEVO_DIFF_ND_WAVES_PER_EU                  // ... of the N-D diff kernel (its resident set)
+#define ASMEVO_DIFF_ND_WAVES_PER_EU 4
 #endif
 #ifndef ASMEVO_COS_WAVES_PER_EU                      // ... and of its cosine variant
 #define ASMEVO_COS_WAVES_PER_EU 3
