@@ -64,6 +64,10 @@ def parse():
     p.add_argument("--cosine-steps", type=int, default=5,
                    help="after the timed steps, time the diff + cosine pass (Eq. 1's c_x) this many "
                         "times on the last candidate and report it beside the metric (0: skip)")
+    p.add_argument("--unplanned-steps", type=int, default=5,
+                   help="after the timed steps (which reuse one staged plan of the state), time the diff + "
+                        "guard check of the last candidate this many times through the unplanned calls "
+                        "(host planning and descriptor upload per check) and report it beside the metric")
     p.add_argument("--nd-steps", type=int, default=3,
                    help="after the timed steps, time N-D views of the two states (sliced rows, a "
                         "permuted 4-D layout, a transposed matrix, a stride-2 gather, narrow half rows, "
@@ -210,6 +214,21 @@ def nd_cases(st, stream, steps: int, scratch):
                      "logical_bytes_per_side": 4 * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
                      "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2)}
         del ws
+        # the same check planned once (asmevo_plan_diff_nd): no planning or upload in the span
+        pws = torch.empty(lib.plan_bytes(n_segs), dtype=torch.uint8, device=st.cand.device)
+        plan = lib.plan_diff_nd(segs, 1, pws.data_ptr(), pws.numel(), stream)
+        times = []
+        for _ in range(steps + 1):
+            if scratch is not None:
+                scratch.fill_(0x76)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            lib.diff_planned(plan, res.data_ptr(), stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        out[name]["planned_ms_median"] = round(statistics.median(times[1:]), 4)
+        del pws
         # the same view with the cosine term (asmevo_diff_cosine_nd: row-tiled walk, block trees)
         cws = torch.empty(lib.diff_cosine_nd_workspace_bytes(segs, 1), dtype=torch.uint8, device=st.cand.device)
         cres = torch.empty(64, dtype=torch.uint8, device=st.cand.device)
@@ -269,14 +288,27 @@ def main():
     flush_mib = args.flush_mib if args.flush_mib >= 0 else (1024 if w.arena_bytes < (4 << 30) else 0)
     scratch = torch.empty(flush_mib << 20, dtype=torch.uint8, device="cuda:0") if flush_mib else None
 
+    # The check of every candidate reuses one staged plan of the state: the
+    # descriptors name the same buffers for every candidate (filled in place),
+    # so they are planned and uploaded once, like the reference fill.
+    planned_steps = args.workgroups == 0
+    if planned_steps:
+        st.plan(stream)
+
     def step(variant, ev):
         st.fill("cand", variant, stream)
         if scratch is not None:
             scratch.fill_(variant & 0xFF)
         ev[0].record(stream)
-        st.diff(stream, args.workgroups)
+        if planned_steps:
+            st.diff_planned(stream)
+        else:
+            st.diff(stream, args.workgroups)
         ev[1].record(stream)
-        st.guard(stream)
+        if planned_steps:
+            st.guard_planned(stream)
+        else:
+            st.guard(stream)
         ev[2].record(stream)
 
     for s in range(args.warmup):
@@ -326,6 +358,28 @@ def main():
                   "min_cosine": min((r["cosine"] for r in floats), default=None),
                   "diff_results_identical": seg_after == results,
                   "note": "one pass: diff + fp64 a*b, a*a, b*b per 4096-byte block, then the block tree"}
+    unplanned = None
+    if args.unplanned_steps > 0:
+        u_dg, u_diff = [], []
+        for _ in range(args.unplanned_steps):
+            if scratch is not None:
+                scratch.fill_(0x3C)
+            torch.cuda.synchronize()
+            pe = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            pe[0].record(stream)
+            st.diff(stream)
+            pe[1].record(stream)
+            st.guard(stream)
+            pe[2].record(stream)
+            torch.cuda.synchronize()
+            u_dg.append(pe[0].elapsed_time(pe[2]))
+            u_diff.append(pe[0].elapsed_time(pe[1]))
+        med_u = statistics.median(u_dg)
+        unplanned = {"diff_guard_ms_median": round(med_u, 4), "diff_ms_median": round(statistics.median(u_diff), 4),
+                     "GBps": round(compared / (med_u * 1e-3) / 1e9, 2),
+                     "results_identical": st.seg_results() == results,
+                     "note": "the same check through the unplanned calls: host planning and a pageable "
+                             "descriptor upload inside every span"}
     restore = None
     if args.restore_steps > 0:
         import paper_2608_20711_amd as lib
@@ -383,8 +437,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": pmc_traffic() if args.workload == "sweep" and not args.small else None,
-                     "kernel": "diff_kernel (event span also holds the descriptor upload and result init)"},
+                     "kernel": "diff_kernel (event span of a planned launch: it also holds the result initialisation)"},
         "diff_cosine": cosine,
+        "unplanned": unplanned,
         "restore": restore,
         "diff_nd": nd,
         "total_mismatches": int(sum(r["mismatches"] for r in results)),

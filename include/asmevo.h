@@ -27,7 +27,9 @@
  *    `segs`) are host memory: they are read and copied during the call, so the
  *    caller may free or reuse them on return.
  *  - `workspace` is device memory of at least asmevo_workspace_bytes(...)
- *    bytes, owned by the caller; the call stages its descriptor tables there.
+ *    bytes, owned by the caller, starting on a 256-byte boundary (as hipMalloc
+ *    and torch allocations do; otherwise ASMEVO_E_INVALID); the call stages
+ *    its descriptor tables there.
  *    It must not be reused by another call until this call's work on `stream`
  *    has completed.  The library allocates no memory of its own, apart from
  *    the asmevo_va_alloc calls, which exist to allocate.
@@ -409,6 +411,51 @@ typedef struct {
 asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
                                  asmevo_guard_result* results,
                                  void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Staged plans (section 3.7, Algorithm 1: eq(c, x) runs for every input x of
+ * every candidate, and section 4.1 repeats each check three times): a diff
+ * or a guard check whose descriptors do not change between calls is planned,
+ * validated and uploaded once, then launched as often as it is repeated with
+ * no host planning and no host-to-device copy per launch.  The plan records
+ * the device addresses its descriptors name: it stays valid while those
+ * buffers and the workspace it was staged in stay allocated and unchanged.
+ *
+ * asmevo_plan_diff / asmevo_plan_guard -- validate exactly as asmevo_diff_
+ * segments / asmevo_guard_check, stage the descriptor table in `workspace`
+ * (at least asmevo_plan_bytes(n) bytes, caller-owned; stream-ordered upload
+ * from pageable memory, synchronous with the host) and fill *plan (host
+ * memory).  Errors as for the unplanned calls; ASMEVO_E_INVALID for a null
+ * plan.
+ * asmevo_plan_diff_nd -- the same for asmevo_diff_segments_nd's segments
+ * and n_results results.
+ * asmevo_diff_planned / asmevo_guard_planned -- enqueue the planned check:
+ * results as the unplanned call's (asmevo_segment_result per result or
+ * asmevo_guard_result per allocation, device memory, initialised
+ * in-stream).  The staged table is only read: launches of one plan may
+ * overlap, each with results of its own.  ASMEVO_E_INVALID for a null or
+ * mismatched plan.
+ */
+enum { ASMEVO_PLAN_DIFF = 1, ASMEVO_PLAN_GUARD = 2, ASMEVO_PLAN_DIFF_ND = 3 };
+typedef struct {
+  uint64_t table;       /* device address of the staged table, inside the plan's workspace */
+  uint64_t units;       /* tiles of the diff, or 16-byte chunks of the guard check */
+  int32_t n;            /* descriptors in the table */
+  int32_t n_results;    /* results one launch writes */
+  int32_t kind;         /* ASMEVO_PLAN_DIFF, ASMEVO_PLAN_DIFF_ND or ASMEVO_PLAN_GUARD */
+  int32_t workgroups;   /* launch width of the diff */
+} asmevo_plan;
+
+size_t asmevo_plan_bytes(int32_t n_descs);
+asmevo_status asmevo_plan_diff(const asmevo_segment* segs, int32_t n, void* workspace, size_t ws_bytes,
+                               void* stream, asmevo_plan* plan);
+asmevo_status asmevo_plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_results, void* workspace,
+                                  size_t ws_bytes, void* stream, asmevo_plan* plan);
+asmevo_status asmevo_diff_planned(const asmevo_plan* plan, asmevo_segment_result* results, void* stream);
+asmevo_status asmevo_plan_guard(const asmevo_alloc* allocs, int32_t n, void* workspace, size_t ws_bytes,
+                                void* stream, asmevo_plan* plan);
+asmevo_status asmevo_guard_planned(const asmevo_plan* plan, uint64_t seed, asmevo_guard_result* results,
+                                   void* stream);
 
 /*
  * One region of a captured pre-dispatch state (section 3.4, Tier 2: the

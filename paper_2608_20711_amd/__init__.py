@@ -112,6 +112,14 @@ class GuardResult(ctypes.Structure):
                 ("bad_pad", ctypes.c_uint64), ("first_bad_pad", ctypes.c_int64)]
 
 
+class Plan(ctypes.Structure):
+    _fields_ = [("table", ctypes.c_uint64), ("units", ctypes.c_uint64), ("n", ctypes.c_int32),
+                ("n_results", ctypes.c_int32), ("kind", ctypes.c_int32), ("workgroups", ctypes.c_int32)]
+
+
+PLAN_DIFF, PLAN_GUARD, PLAN_DIFF_ND = 1, 2, 3
+
+
 class Kernel(ctypes.Structure):
     _fields_ = [("module", ctypes.c_uint64), ("function", ctypes.c_uint64), ("num_regs", ctypes.c_int32),
                 ("shared_bytes", ctypes.c_int32), ("max_threads", ctypes.c_int32), ("local_bytes", ctypes.c_int32)]
@@ -127,7 +135,8 @@ EXPORTED = ["asmevo_fill_guarded", "asmevo_diff_segments", "asmevo_diff_segments
             "asmevo_diff_nd_workspace_bytes", "asmevo_kernel_load", "asmevo_kernel_unload",
             "asmevo_kernel_launch", "asmevo_kernel_time", "asmevo_va_granularity", "asmevo_va_alloc",
             "asmevo_va_free", "asmevo_diff_cosine_nd", "asmevo_diff_cosine_nd_workspace_bytes",
-            "asmevo_diff_segments_noalloc"]
+            "asmevo_diff_segments_noalloc", "asmevo_plan_bytes", "asmevo_plan_diff", "asmevo_diff_planned",
+            "asmevo_plan_guard", "asmevo_guard_planned", "asmevo_plan_diff_nd"]
 
 
 class AsmevoError(RuntimeError):
@@ -163,6 +172,19 @@ def _lib() -> ctypes.CDLL:
         L.asmevo_diff_segments_ex.restype = ctypes.c_int32
         L.asmevo_diff_segments_noalloc.argtypes = [P(Segment), ctypes.c_int32, vp, vp]
         L.asmevo_diff_segments_noalloc.restype = ctypes.c_int32
+        L.asmevo_plan_bytes.argtypes = [ctypes.c_int32]
+        L.asmevo_plan_bytes.restype = ctypes.c_size_t
+        L.asmevo_plan_diff.argtypes = [P(Segment), ctypes.c_int32, vp, ctypes.c_size_t, vp, P(Plan)]
+        L.asmevo_plan_diff.restype = ctypes.c_int32
+        L.asmevo_plan_diff_nd.argtypes = [P(SegmentND), ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t, vp,
+                                          P(Plan)]
+        L.asmevo_plan_diff_nd.restype = ctypes.c_int32
+        L.asmevo_diff_planned.argtypes = [P(Plan), vp, vp]
+        L.asmevo_diff_planned.restype = ctypes.c_int32
+        L.asmevo_plan_guard.argtypes = [P(Alloc), ctypes.c_int32, vp, ctypes.c_size_t, vp, P(Plan)]
+        L.asmevo_plan_guard.restype = ctypes.c_int32
+        L.asmevo_guard_planned.argtypes = [P(Plan), ctypes.c_uint64, vp, vp]
+        L.asmevo_guard_planned.restype = ctypes.c_int32
         L.asmevo_diff_cosine.argtypes = [P(Segment), ctypes.c_int32, vp, vp, vp, ctypes.c_size_t, vp]
         L.asmevo_diff_cosine.restype = ctypes.c_int32
         L.asmevo_diff_segments_nd.argtypes = [P(SegmentND), ctypes.c_int32, vp, ctypes.c_int32, vp,
@@ -272,6 +294,48 @@ def diff_segments_noalloc(segments: Sequence[Segment], results_ptr: int, stream=
     s = _array(Segment, segments)
     _check(_lib().asmevo_diff_segments_noalloc(s, len(segments), results_ptr, _stream_handle(stream)),
            "asmevo_diff_segments_noalloc")
+
+
+def plan_bytes(n_descs: int) -> int:
+    return int(_lib().asmevo_plan_bytes(n_descs))
+
+
+def plan_diff(segments: Sequence[Segment], workspace_ptr: int, workspace_size: int, stream=None) -> Plan:
+    """Stages the segments' descriptor table once (asmevo_plan_diff)."""
+    plan = Plan()
+    s = _array(Segment, segments)
+    _check(_lib().asmevo_plan_diff(s, len(segments), workspace_ptr, workspace_size, _stream_handle(stream),
+                                   ctypes.byref(plan)), "asmevo_plan_diff")
+    return plan
+
+
+def plan_diff_nd(segments: Sequence[SegmentND], n_results: int, workspace_ptr: int, workspace_size: int,
+                 stream=None) -> Plan:
+    """Stages N-D segments' descriptor table once (asmevo_plan_diff_nd)."""
+    plan = Plan()
+    s = _array(SegmentND, segments)
+    _check(_lib().asmevo_plan_diff_nd(s, len(segments), n_results, workspace_ptr, workspace_size,
+                                      _stream_handle(stream), ctypes.byref(plan)), "asmevo_plan_diff_nd")
+    return plan
+
+
+def diff_planned(plan: Plan, results_ptr: int, stream=None) -> None:
+    _check(_lib().asmevo_diff_planned(ctypes.byref(plan), results_ptr, _stream_handle(stream)),
+           "asmevo_diff_planned")
+
+
+def plan_guard(allocs: Sequence[Alloc], workspace_ptr: int, workspace_size: int, stream=None) -> Plan:
+    """Stages the guard regions of the allocations once (asmevo_plan_guard)."""
+    plan = Plan()
+    a = _array(Alloc, allocs)
+    _check(_lib().asmevo_plan_guard(a, len(allocs), workspace_ptr, workspace_size, _stream_handle(stream),
+                                    ctypes.byref(plan)), "asmevo_plan_guard")
+    return plan
+
+
+def guard_planned(plan: Plan, seed: int, results_ptr: int, stream=None) -> None:
+    _check(_lib().asmevo_guard_planned(ctypes.byref(plan), seed, results_ptr, _stream_handle(stream)),
+           "asmevo_guard_planned")
 
 
 def diff_nd_workspace_bytes(n: int) -> int:

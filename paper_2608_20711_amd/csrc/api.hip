@@ -51,6 +51,11 @@ bool is_float(uint32_t dtype) { return dtype >= ASMEVO_F32 && dtype <= ASMEVO_FP
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Workspaces start on a 256-byte boundary (as hipMalloc and torch
+// allocations do): the kernels' 64-bit atomics on counters and accumulators
+// staged there need natural alignment.
+bool ws_aligned(const void* workspace) { return (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0; }
+
 uint64_t data_bytes(const asmevo_alloc& A) {
   if (A.rows <= 0 || A.cols <= 0) return 0;
   return (uint64_t)((A.rows - 1) * A.stride + A.cols) * (uint64_t)esize_of(A.dtype);
@@ -273,6 +278,7 @@ asmevo_status asmevo_fill_guarded(const asmevo_alloc* allocs, int32_t n,
   const size_t off_pts = off_rules + align256(rules.size() * sizeof(FillRule));
   const size_t bytes = off_pts + points.size() * sizeof(PointEntry);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   std::vector<uint8_t> host(bytes, 0);
   put(host, 0, dev);
   put(host, off_rules, rules);
@@ -632,6 +638,7 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
   if (st != ASMEVO_OK) return st;
   const size_t bytes = dev.size() * sizeof(DiffSeg);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
   int wg = workgroups;
@@ -726,6 +733,7 @@ asmevo_status asmevo_diff_segments_nd(const asmevo_segment_nd* segs, int32_t n,
   uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
   if (n > 0) {
     if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+    if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
     std::vector<uint8_t> host(bytes, 0);
     put(host, 0, dev);
     put(host, off_ext, ext);
@@ -758,6 +766,7 @@ asmevo_status asmevo_diff_cosine(const asmevo_segment* segs, int32_t n,
   for (const CosLevels& L : P.lv)     // the final fold stages at most 255 entries per level
     if (L.cnt[kCosLevels - 1] > 255) return ASMEVO_E_UNSUPPORTED;
   if (!workspace || ws_bytes < P.bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
   HIP_TRY(hipMemcpyAsync(ws, dev.data(), dev.size() * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
@@ -792,6 +801,7 @@ asmevo_status asmevo_diff_cosine_nd(const asmevo_segment_nd* segs, int32_t n, as
   if (st != ASMEVO_OK) return st;
   if (n_results == 0) return ASMEVO_OK;
   if (!workspace || ws_bytes < P.bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
   const CosPlan& C = P.cos;
@@ -863,6 +873,7 @@ asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n, void*
   }
   const size_t bytes = dev.size() * sizeof(CopyRegion);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
   // two workgroups per CU, each streaming one range with its four waves: of
@@ -873,14 +884,16 @@ asmevo_status asmevo_copy_regions(const asmevo_region* regions, int32_t n, void*
 }
 
 // ---------------------------------------------------------------------------
-asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
-                                 asmevo_guard_result* results, void* workspace, size_t ws_bytes,
-                                 void* stream) {
-  if (n < 0 || (n > 0 && (!allocs || !results))) return ASMEVO_E_INVALID;
-  if (n > (1 << 29)) return ASMEVO_E_INVALID;   // result index and guard side share a 32-bit key
-  if (n == 0) return ASMEVO_OK;
-  std::vector<GuardRegion> regs;
-  uint64_t chunks = 0;
+}  // extern "C"
+
+namespace {
+
+// Validates the allocations and builds the guard regions: each guard side,
+// and the row padding of a strided allocation as one region of runs.
+asmevo_status plan_guard(const asmevo_alloc* allocs, int32_t n, std::vector<GuardRegion>& regs,
+                         uint64_t& chunks) {
+  regs.clear();
+  chunks = 0;
   for (int32_t k = 0; k < n; ++k) {
     const asmevo_alloc& A = allocs[k];
     asmevo_status st = check_alloc_geometry(A);
@@ -919,14 +932,152 @@ asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t
       chunks += (uint64_t)(A.rows - 1) * R.run_chunks;
     }
   }
+  return ASMEVO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+asmevo_status asmevo_guard_check(const asmevo_alloc* allocs, int32_t n, uint64_t seed,
+                                 asmevo_guard_result* results, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  if (n < 0 || (n > 0 && (!allocs || !results))) return ASMEVO_E_INVALID;
+  if (n > (1 << 29)) return ASMEVO_E_INVALID;   // result index and guard side share a 32-bit key
+  if (n == 0) return ASMEVO_OK;
+  std::vector<GuardRegion> regs;
+  uint64_t chunks = 0;
+  asmevo_status st = plan_guard(allocs, n, regs, chunks);
+  if (st != ASMEVO_OK) return st;
   const size_t bytes = std::max<size_t>(regs.size(), 1) * sizeof(GuardRegion);
   if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+  if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (!regs.empty())
     HIP_TRY(hipMemcpyAsync(workspace, regs.data(), regs.size() * sizeof(GuardRegion),
                            hipMemcpyHostToDevice, s));
   HIP_TRY(launch_guard(reinterpret_cast<const GuardRegion*>(workspace), (int)regs.size(), chunks,
                        seed, results, n, s));
+  return ASMEVO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Staged plans: the descriptor table of a diff or guard check is planned and
+// uploaded once, then launched as often as the check is repeated.
+
+size_t asmevo_plan_bytes(int32_t n_descs) {
+  const size_t n = n_descs > 0 ? (size_t)n_descs : 0;
+  // the largest table: N-D segments with extensions, or up to 3 guard regions per allocation
+  return align256(std::max(n * sizeof(DiffSeg), 3 * n * sizeof(GuardRegion))) + align256(n * sizeof(NdExt)) + 256;
+}
+
+asmevo_status asmevo_plan_diff(const asmevo_segment* segs, int32_t n, void* workspace, size_t ws_bytes,
+                               void* stream, asmevo_plan* plan) {
+  if (!plan || n < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
+  std::vector<DiffSeg> dev((size_t)n);
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff(segs, n, false, dev.data(), tiles);
+  if (st != ASMEVO_OK) return st;
+  const size_t bytes = dev.size() * sizeof(DiffSeg);
+  if (n > 0) {
+    if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+    if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
+    HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice,
+                           reinterpret_cast<hipStream_t>(stream)));
+  }
+  std::memset(plan, 0, sizeof(*plan));
+  plan->table = reinterpret_cast<uint64_t>(workspace);
+  plan->units = tiles;
+  plan->n = n;
+  plan->n_results = n;
+  plan->kind = ASMEVO_PLAN_DIFF;
+  plan->workgroups = diff_workgroups(tiles);
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_results, void* workspace,
+                                  size_t ws_bytes, void* stream, asmevo_plan* plan) {
+  if (!plan || n < 0 || n_results < 0 || (n > 0 && !segs)) return ASMEVO_E_INVALID;
+  std::vector<DiffSeg> dev;
+  std::vector<NdExt> ext;
+  uint64_t tiles = 0;
+  asmevo_status st = plan_diff_nd(segs, n, n_results, dev, ext, tiles);
+  if (st != ASMEVO_OK) return st;
+  const size_t off_ext = align256(dev.size() * sizeof(DiffSeg));
+  const size_t bytes = off_ext + ext.size() * sizeof(NdExt);
+  if (n > 0) {
+    if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+    if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
+    std::vector<uint8_t> host(bytes, 0);
+    put(host, 0, dev);
+    put(host, off_ext, ext);
+    HIP_TRY(hipMemcpyAsync(workspace, host.data(), bytes, hipMemcpyHostToDevice,
+                           reinterpret_cast<hipStream_t>(stream)));
+  }
+  std::memset(plan, 0, sizeof(*plan));
+  plan->table = reinterpret_cast<uint64_t>(workspace);
+  plan->units = tiles;
+  plan->n = n;
+  plan->n_results = n_results;
+  plan->kind = ASMEVO_PLAN_DIFF_ND;
+  plan->workgroups = device_cus() * diff_nd_blocks_per_cu();
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_diff_planned(const asmevo_plan* plan, asmevo_segment_result* results, void* stream) {
+  if (!plan || plan->n < 0 || plan->n_results < 0) return ASMEVO_E_INVALID;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (plan->kind == ASMEVO_PLAN_DIFF) {
+    if (plan->n != plan->n_results || (plan->n > 0 && (!results || !plan->table))) return ASMEVO_E_INVALID;
+    if (plan->n == 0) return ASMEVO_OK;
+    HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(plan->table), plan->n, plan->units, results,
+                        plan->workgroups, s));
+    return ASMEVO_OK;
+  }
+  if (plan->kind == ASMEVO_PLAN_DIFF_ND) {
+    if ((plan->n_results > 0 && !results) || (plan->n > 0 && !plan->table)) return ASMEVO_E_INVALID;
+    if (plan->n_results == 0) return ASMEVO_OK;
+    const uint8_t* ws = reinterpret_cast<const uint8_t*>(plan->table);
+    const size_t off_ext = align256((size_t)plan->n * sizeof(DiffSeg));
+    HIP_TRY(launch_diff_nd(reinterpret_cast<const DiffSeg*>(ws), reinterpret_cast<const NdExt*>(ws + off_ext),
+                           plan->n, plan->n_results, plan->units, results, plan->workgroups, s));
+    return ASMEVO_OK;
+  }
+  return ASMEVO_E_INVALID;
+}
+
+asmevo_status asmevo_plan_guard(const asmevo_alloc* allocs, int32_t n, void* workspace, size_t ws_bytes,
+                                void* stream, asmevo_plan* plan) {
+  if (!plan || n < 0 || (n > 0 && !allocs)) return ASMEVO_E_INVALID;
+  if (n > (1 << 29)) return ASMEVO_E_INVALID;
+  std::vector<GuardRegion> regs;
+  uint64_t chunks = 0;
+  asmevo_status st = plan_guard(allocs, n, regs, chunks);
+  if (st != ASMEVO_OK) return st;
+  const size_t bytes = regs.size() * sizeof(GuardRegion);
+  if (!regs.empty()) {
+    if (!workspace || ws_bytes < bytes) return ASMEVO_E_WORKSPACE;
+    if (!ws_aligned(workspace)) return ASMEVO_E_INVALID;
+    HIP_TRY(hipMemcpyAsync(workspace, regs.data(), bytes, hipMemcpyHostToDevice,
+                           reinterpret_cast<hipStream_t>(stream)));
+  }
+  std::memset(plan, 0, sizeof(*plan));
+  plan->table = reinterpret_cast<uint64_t>(workspace);
+  plan->units = chunks;
+  plan->n = (int32_t)regs.size();
+  plan->n_results = n;
+  plan->kind = ASMEVO_PLAN_GUARD;
+  return ASMEVO_OK;
+}
+
+asmevo_status asmevo_guard_planned(const asmevo_plan* plan, uint64_t seed, asmevo_guard_result* results,
+                                   void* stream) {
+  if (!plan || plan->kind != ASMEVO_PLAN_GUARD || plan->n < 0 || plan->n_results < 0 ||
+      (plan->n_results > 0 && !results) || (plan->n > 0 && !plan->table))
+    return ASMEVO_E_INVALID;
+  if (plan->n_results == 0) return ASMEVO_OK;
+  HIP_TRY(launch_guard(reinterpret_cast<const GuardRegion*>(plan->table), plan->n, plan->units, seed, results,
+                       plan->n_results, reinterpret_cast<hipStream_t>(stream)));
   return ASMEVO_OK;
 }
 

@@ -12,7 +12,7 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (Alloc, DIST_CODE, DTYPE_CODE, FILL_SATURATE, Injection, KIND_CODE, MODE_CODE,
+from . import (Alloc, DIST_CODE, diff_planned, guard_planned, plan_bytes, plan_diff, plan_guard, DTYPE_CODE, FILL_SATURATE, Injection, KIND_CODE, MODE_CODE,
                NAN_CODE, INJ_RATE, SIDE_CODE, Segment, descriptor_array, diff_cosine,
                diff_cosine_workspace_bytes, diff_segments, fill_guarded, guard_check, workspace_bytes)
 
@@ -110,6 +110,21 @@ class DeviceState:
         n = len(self.w.compares)
         raw = self.cos_res.cpu().numpy()[: n * COS_RESULT_DTYPE.itemsize].view(COS_RESULT_DTYPE)
         return [{f: raw[f][k].item() for f in COS_RESULT_DTYPE.names} for k in range(n)]
+
+    def plan(self, stream=None) -> None:
+        """Stages the diff's and the guard check's tables once (repeated checks
+        then launch without host planning or uploads)."""
+        n = max(len(self.w.compares), len(self.w.allocs))
+        size = -(-plan_bytes(n) // 256) * 256        # each plan's workspace starts on a 256-byte boundary
+        self.plan_ws = torch.empty(2 * size, dtype=torch.uint8, device=self.device)
+        self.diff_plan = plan_diff(self.segments, self.plan_ws.data_ptr(), size, stream)
+        self.guard_plan = plan_guard(self.allocs_cand, self.plan_ws.data_ptr() + size, size, stream)
+
+    def diff_planned(self, stream=None) -> None:
+        diff_planned(self.diff_plan, self.seg_res.data_ptr(), stream)
+
+    def guard_planned(self, stream=None) -> None:
+        guard_planned(self.guard_plan, self.w.seed, self.guard_res.data_ptr(), stream)
 
     def guard(self, stream=None) -> None:
         guard_check(self.allocs_cand, self.w.seed, self.guard_res.data_ptr(), self.ws.data_ptr(),

@@ -39,7 +39,7 @@ def test_struct_layouts_match_header(tmp_path):
         "asmevo_alloc": lib.Alloc, "asmevo_injection": lib.Injection, "asmevo_segment": lib.Segment,
         "asmevo_segment_result": lib.SegmentResult, "asmevo_guard_result": lib.GuardResult,
         "asmevo_cosine_result": lib.CosineResult, "asmevo_region": lib.Region,
-        "asmevo_segment_nd": lib.SegmentND,
+        "asmevo_segment_nd": lib.SegmentND, "asmevo_plan": lib.Plan,
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "asmevo.h"', "int main(void) {"]
     for cname, cls in fields.items():
@@ -302,3 +302,51 @@ def test_noalloc_diff_argument_errors():
     assert L.asmevo_diff_segments_noalloc(bad, 1, 0x1000, None) == lib.E_INVALID
     assert L.asmevo_diff_segments_noalloc(arr, 0, 0x1000, None) == lib.OK
     assert b"static" in L.asmevo_status_string(lib.E_CAPACITY)
+
+
+def test_plan_argument_errors_before_any_device_work():
+    """Plans validate like the unplanned calls, before anything is enqueued;
+    a planned launch refuses a null or mismatched plan."""
+    L = lib.lib()
+    plan = lib.Plan()
+    bad = (lib.Segment * 1)(_seg(stride_a=1, cols=5))
+    assert L.asmevo_plan_diff(bad, 1, 0x40000, 1 << 20, None, ctypes.byref(plan)) == lib.E_INVALID
+    good = (lib.Segment * 1)(_seg())
+    assert L.asmevo_plan_diff(good, 1, 0x40000, 1 << 20, None, None) == lib.E_INVALID
+    assert L.asmevo_plan_diff(good, 1, 0x40000, 8, None, ctypes.byref(plan)) == lib.E_WORKSPACE
+    assert L.asmevo_plan_diff(good, 1, None, 1 << 20, None, ctypes.byref(plan)) == lib.E_WORKSPACE
+    allocs = (lib.Alloc * 1)(_alloc(stride=10))
+    assert L.asmevo_plan_guard(allocs, 1, 0x40000, 1 << 20, None, ctypes.byref(plan)) == lib.E_INVALID
+    assert L.asmevo_diff_planned(None, 0x1000, None) == lib.E_INVALID
+    p = lib.Plan(0x40000, 4, 1, 1, lib.PLAN_GUARD, 256)
+    assert L.asmevo_diff_planned(ctypes.byref(p), 0x1000, None) == lib.E_INVALID       # a guard plan
+    p = lib.Plan(0x40000, 4, 1, 1, lib.PLAN_DIFF, 256)
+    assert L.asmevo_guard_planned(ctypes.byref(p), 1, 0x1000, None) == lib.E_INVALID   # a diff plan
+    assert L.asmevo_diff_planned(ctypes.byref(p), None, None) == lib.E_INVALID
+    empty = lib.Plan(0, 0, 0, 0, lib.PLAN_DIFF, 0)
+    assert L.asmevo_diff_planned(ctypes.byref(empty), None, None) == lib.OK
+    assert L.asmevo_plan_bytes(4096) >= 4096 * (128 + 328) and L.asmevo_plan_bytes(100) >= 300 * 64
+    nd = (lib.SegmentND * 1)(_seg_nd(index_base=-5))
+    assert L.asmevo_plan_diff_nd(nd, 1, 1, 0x40000, 1 << 20, None, ctypes.byref(plan)) == lib.E_INVALID
+    nd = (lib.SegmentND * 1)(_seg_nd())
+    assert L.asmevo_plan_diff_nd(nd, 1, 1, 0x40000, 8, None, ctypes.byref(plan)) == lib.E_WORKSPACE
+    p = lib.Plan(0x40000, 4, 1, 0, lib.PLAN_DIFF_ND, 256)
+    assert L.asmevo_diff_planned(ctypes.byref(p), None, None) == lib.OK               # no results: nothing to do
+    p = lib.Plan(0x40000, 4, 1, 2, lib.PLAN_DIFF_ND, 256)
+    assert L.asmevo_diff_planned(ctypes.byref(p), None, None) == lib.E_INVALID
+    p = lib.Plan(0x40000, 4, 1, 1, 9, 256)
+    assert L.asmevo_diff_planned(ctypes.byref(p), 0x1000, None) == lib.E_INVALID      # unknown kind
+
+
+def test_workspace_must_be_256_byte_aligned():
+    """Workspaces start on a 256-byte boundary (kernels keep 64-bit atomic
+    counters there): a misaligned one is refused before anything is enqueued."""
+    L = lib.lib()
+    segs = (lib.Segment * 1)(_seg())
+    assert L.asmevo_diff_segments(segs, 1, 0x1000, 0x40008, 1 << 20, None) == lib.E_INVALID
+    plan = lib.Plan()
+    assert L.asmevo_plan_diff(segs, 1, 0x40010, 1 << 20, None, ctypes.byref(plan)) == lib.E_INVALID
+    allocs = (lib.Alloc * 1)(_alloc())
+    assert L.asmevo_plan_guard(allocs, 1, 0x40104, 1 << 20, None, ctypes.byref(plan)) == lib.E_INVALID
+    assert L.asmevo_guard_check(allocs, 1, 7, 0x1000, 0x40040, 1 << 20, None) == lib.E_INVALID
+    assert L.asmevo_diff_cosine(segs, 1, 0x1000, 0x2000, 0x40080, 1 << 20, None) == lib.E_INVALID
