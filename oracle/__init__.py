@@ -156,6 +156,8 @@ def lib() -> ctypes.CDLL:
         L.ref_sincos_turns_n.argtypes = [vp, ctypes.c_int64, vp, vp]
         L.ref_normal_n.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int, vp]
         L.ref_philox_n.argtypes = [vp, vp, ctypes.c_int64, vp]
+        L.ref_compare_pair_n.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                         ctypes.c_double, vp, vp, ctypes.c_int64, vp, vp, vp]
         _lib_handle = L
     return _lib_handle
 
@@ -193,34 +195,57 @@ def decode_n(dtype: str, raw: np.ndarray):
     return cls, val
 
 
-def encode_f32_n(dtype: str, x: np.ndarray, saturate: bool = False) -> np.ndarray:
+def _out(out, shape, dtype):
+    """A caller's output array (contiguous, of the right type and size), or a new one."""
+    if out is None:
+        return np.zeros(shape, dtype=dtype)
+    assert out.dtype == dtype and out.flags.c_contiguous and out.shape == shape
+    return out
+
+
+def encode_f32_n(dtype: str, x: np.ndarray, saturate: bool = False, out=None) -> np.ndarray:
     x = np.ascontiguousarray(x, dtype=np.float32)
-    out = np.zeros(x.shape, dtype=np.uint64)
+    out = _out(out, x.shape, np.uint64)
     lib().ref_encode_f32_n(DTYPE[dtype], _ptr(x), x.size, int(saturate), _ptr(out))
     return out
 
 
-def log_u_n(x: np.ndarray) -> np.ndarray:
+def log_u_n(x: np.ndarray, out=None) -> np.ndarray:
     x = np.ascontiguousarray(x, dtype=np.uint32)
-    out = np.zeros(x.shape, dtype=np.float64)
+    out = _out(out, x.shape, np.float64)
     lib().ref_log_u_n(_ptr(x), x.size, _ptr(out))
     return out
 
 
-def sincos_turns_n(x: np.ndarray):
+def sincos_turns_n(x: np.ndarray, c=None, s=None):
     x = np.ascontiguousarray(x, dtype=np.uint32)
-    c = np.zeros(x.shape, dtype=np.float64)
-    s = np.zeros(x.shape, dtype=np.float64)
+    c = _out(c, x.shape, np.float64)
+    s = _out(s, x.shape, np.float64)
     lib().ref_sincos_turns_n(_ptr(x), x.size, _ptr(c), _ptr(s))
     return c, s
 
 
-def normal_n(xa: np.ndarray, xb: np.ndarray, which: int) -> np.ndarray:
+def normal_n(xa: np.ndarray, xb: np.ndarray, which: int, out=None) -> np.ndarray:
     xa = np.ascontiguousarray(xa, dtype=np.uint32)
     xb = np.ascontiguousarray(xb, dtype=np.uint32)
-    out = np.zeros(xa.shape, dtype=np.float64)
+    out = _out(out, xa.shape, np.float64)
     lib().ref_normal_n(_ptr(xa), _ptr(xb), xa.size, which, _ptr(out))
     return out
+
+
+def compare_pair_n(dtype: str, mode: str, nan_policy: str, atol: float, rtol: float,
+                   ra: np.ndarray, rb: np.ndarray, flags=None, max_abs=None, max_rel=None):
+    """Each pair compared on its own: (flags, max_abs, max_rel) with flags bit 0
+    a bitwise difference, bit 1 a mismatch, bit 2 a non-finite mismatch."""
+    ra = np.ascontiguousarray(ra, dtype=np.uint64)
+    rb = np.ascontiguousarray(rb, dtype=np.uint64)
+    assert ra.shape == rb.shape
+    flags = _out(flags, ra.shape, np.uint8)
+    max_abs = _out(max_abs, ra.shape, np.float64)
+    max_rel = _out(max_rel, ra.shape, np.float64)
+    lib().ref_compare_pair_n(DTYPE[dtype], MODE[mode], NAN_POLICY[nan_policy], atol, rtol, _ptr(ra), _ptr(rb),
+                             ra.size, _ptr(flags), _ptr(max_abs), _ptr(max_rel))
+    return flags, max_abs, max_rel
 
 
 def canary_byte(seed: int, alloc_id: int, side: int, p: int) -> int:

@@ -984,3 +984,17 @@ void ref_normal_n(const uint32_t* xa, const uint32_t* xb, int64_t n, int which, 
 void ref_philox_n(const uint32_t* ctr, const uint32_t* key, int64_t n, uint32_t* out) {
   for (int64_t k = 0; k < n; ++k) ref_philox4x32_10(ctr + 4 * k, key + 2 * k, out + 4 * k);
 }
+
+void ref_compare_pair_n(int32_t dtype, int32_t mode, int32_t nan_policy, double atol, double rtol,
+                        const uint64_t* ra, const uint64_t* rb, int64_t n, uint8_t* flags,
+                        double* max_abs, double* max_rel) {
+  for (int64_t k = 0; k < n; ++k) {
+    ref_seg_result r;
+    result_reset(&r);
+    compare_pair(dtype, mode, nan_policy, atol, rtol, ra[k], rb[k], 0, &r);
+    flags[k] = (uint8_t)((r.bitwise_mismatches != 0) | ((r.mismatches != 0) << 1) |
+                         ((r.nonfinite_mismatches != 0) << 2));
+    max_abs[k] = r.max_abs;
+    max_rel[k] = r.max_rel;
+  }
+}

@@ -175,6 +175,12 @@ void ref_log_u_n(const uint32_t* x, int64_t n, double* out);
 void ref_sincos_turns_n(const uint32_t* x, int64_t n, double* c, double* s);
 void ref_normal_n(const uint32_t* xa, const uint32_t* xb, int64_t n, int which, double* out);
 void ref_philox_n(const uint32_t* ctr, const uint32_t* key, int64_t n, uint32_t* out);
+/* Each pair (ra[k], rb[k]) compared on its own as a one-element segment:
+ * flags bit 0 bitwise difference, bit 1 mismatch, bit 2 non-finite mismatch;
+ * max_abs / max_rel the segment's maxima (0 unless finite with differing bits). */
+void ref_compare_pair_n(int32_t dtype, int32_t mode, int32_t nan_policy, double atol, double rtol,
+                        const uint64_t* ra, const uint64_t* rb, int64_t n, uint8_t* flags,
+                        double* max_abs, double* max_rel);
 
 #ifdef __cplusplus
 }

@@ -286,3 +286,35 @@ def test_guard_check_every_byte_of_tiny_guards():
     # another seed or buffer id gives other canaries
     assert oracle.guard_check(seed + 1, aid, lo, hi)["bad_lo"] > n // 2
     assert oracle.guard_check(seed, aid + 1, lo, hi)["bad_lo"] > n // 2
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16", "fp8e4m3"])
+@pytest.mark.parametrize("policy", ["equal", "strict"])
+def test_pairwise_bulk_equals_one_element_segments_and_numpy(dtype, policy):
+    """The bulk per-pair loop (what the GPU's per-pair rule is compared with,
+    pair by pair) against one-element segments of the oracle's own diff, and
+    against numpy: isclose for the outcome, fp64 |A - B| and |A - B| / |B| for
+    the maxima of finite pairs whose bits differ."""
+    rng = np.random.default_rng(31)
+    bits = 8 * ESIZE[dtype]
+    a = rng.integers(0, 1 << bits, size=3000, dtype=np.uint64)
+    b = a.copy()
+    b[0::3] ^= np.uint64(1) << rng.integers(0, bits, size=b[0::3].size).astype(np.uint64)
+    b[1::3] = rng.integers(0, 1 << bits, size=b[1::3].size, dtype=np.uint64)
+    atol, rtol = 1e-3, 2.0 ** -7
+    flags, mabs, mrel = oracle.compare_pair_n(dtype, "tolerance", policy, atol, rtol, a, b)
+    for k in range(0, a.size, 7):
+        r = _diff(dtype, a[k:k + 1], b[k:k + 1], policy=policy, atol=atol, rtol=rtol)
+        assert flags[k] == (r["bitwise_mismatches"] | r["mismatches"] << 1 | r["nonfinite_mismatches"] << 2)
+        assert (mabs[k], mrel[k]) == (r["max_abs"], r["max_rel"])
+    mism, A, B = _expected_from_isclose(dtype, a, b, atol, rtol, policy == "equal")
+    if policy == "strict":
+        mism = mism | np.isnan(B)
+    assert np.array_equal((flags >> 1) & 1, mism.astype(np.uint8))
+    assert np.array_equal(flags & 1, (a != b).astype(np.uint8))
+    fin = np.isfinite(A) & np.isfinite(B) & (a != b)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        d = np.abs(A - B)
+        rel = np.where(B != 0, d / np.abs(B), np.where(d == 0, 0.0, np.inf))
+    assert np.array_equal(mabs, np.where(fin, d, 0.0))
+    assert np.array_equal(mrel, np.where(fin, rel, 0.0))
