@@ -41,7 +41,7 @@ def pmc_traffic():
     except (OSError, StopIteration, ValueError):
         return None
     h = hashlib.sha256()
-    for f in ("diff.hip", "layout.h", "device_math.h"):
+    for f in ("diff.hip", "layout.h", "device_math.h", "pair_rule.h"):
         with open(os.path.join(ROOT, "paper_2608_20711_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return rec["bytes_per_launch"] if h.hexdigest() == rec["source_sha256"] else None
