@@ -28,6 +28,8 @@ if ROOT not in sys.path:
 METRIC = "compared bytes/sec (GB/s) of segmented diff + guard check; % of HBM peak"
 HBM_PEAK_GBPS = 8000.0
 CPU_THREADS = 16
+# the sources of the diff kernel that the committed counter summary was taken with
+PROFILED_SOURCES = ("diff.hip", "layout.h", "device_math.h", "pair_rule.h")
 
 
 def pmc_traffic():
@@ -41,9 +43,12 @@ def pmc_traffic():
     except (OSError, StopIteration, ValueError):
         return None
     h = hashlib.sha256()
-    for f in ("diff.hip", "layout.h", "device_math.h", "pair_rule.h"):
-        with open(os.path.join(ROOT, "paper_2608_20711_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    try:
+        for f in PROFILED_SOURCES:
+            with open(os.path.join(ROOT, "paper_2608_20711_amd", "csrc", f), "rb") as fh:
+                h.update(fh.read())
+    except OSError:
+        return None
     return rec["bytes_per_launch"] if h.hexdigest() == rec["source_sha256"] else None
 
 

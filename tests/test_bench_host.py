@@ -22,8 +22,8 @@ def test_more_than_one_gpu_is_refused():
 
 def _tree(tmp_path):
     """A copy of the files pmc_traffic reads."""
-    for rel in ("profiles/diff_kernel_sweep_pmc.md", "paper_2608_20711_amd/csrc/diff.hip",
-                "paper_2608_20711_amd/csrc/layout.h", "paper_2608_20711_amd/csrc/device_math.h"):
+    for rel in ("profiles/diff_kernel_sweep_pmc.md",
+                *("paper_2608_20711_amd/csrc/" + f for f in bench.PROFILED_SOURCES)):
         dst = tmp_path / rel
         dst.parent.mkdir(parents=True, exist_ok=True)
         shutil.copy(os.path.join(ROOT, rel), dst)
@@ -44,5 +44,7 @@ def test_traffic_only_while_the_profiled_sources_are_unchanged(tmp_path, monkeyp
     with open(root / "paper_2608_20711_amd/csrc/diff.hip", "a") as f:
         f.write("\n// changed\n")
     assert bench.pmc_traffic() is None            # a changed kernel source voids the figure
+    os.remove(root / "paper_2608_20711_amd/csrc/diff.hip")
+    assert bench.pmc_traffic() is None            # so does a missing one
     (root / "profiles/diff_kernel_sweep_pmc.md").write_text("no summary here\n")
     assert bench.pmc_traffic() is None
