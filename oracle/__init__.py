@@ -23,7 +23,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ref_oracle.c")
-_SO = os.path.join(_HERE, "libref_oracle.so")
+_SO = os.environ.get("REF_ORACLE_LIBRARY") or os.path.join(_HERE, "libref_oracle.so")
 
 # codes of ref_oracle.h
 DTYPE = {"f32": 1, "bf16": 2, "f16": 3, "fp8e4m3": 4, "i32": 5, "i64": 6, "u8": 7}

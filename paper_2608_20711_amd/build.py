@@ -42,9 +42,10 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    """Compiles every HIP source (in parallel) and links libasmevo.so (always recompiles)."""
-    tmp = LIB + ".tmp"
+def build(verbose: bool = False, extra=(), out: str = LIB) -> str:
+    """Compiles every HIP source (in parallel) and links libasmevo.so, or the
+    library `out` (always recompiles)."""
+    tmp = out + ".tmp"
     compile_flags = [f for f in FLAGS if f != "-shared"]
     with tempfile.TemporaryDirectory() as objdir:
         jobs, objs = [], []
@@ -63,8 +64,8 @@ def build(verbose: bool = False, extra=()) -> str:
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 def build_probe(verbose: bool = False) -> str:
