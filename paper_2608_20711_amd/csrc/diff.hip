@@ -1066,6 +1066,41 @@ __device__ __forceinline__ uint64_t wave_max(uint64_t v) {
 
 // Folds the wave's partials for one segment into its result (only if the
 // wave saw anything) and resets them.
+// Adds a wave's partials for segment S to its result: counts added, first
+// indices min'd, the non-negative maxima max'd as bit patterns, all with
+// exact 64-bit atomics; fields with nothing to add are skipped.  VEC: the
+// seven fields go as three vector atomics from lanes 0-2 (one per
+// operation: counts at words 0, 2, 4, first indices at 1, 3, maxima at 5, 6)
+// instead of seven from lane 0 -- on one result's cache line each atomic is
+// serialised, and the 2-D kernels' flushes meet there when a difference sits
+// in nearly every tile (the N-D variants keep lane 0, for want of
+// registers).
+__device__ __forceinline__ void add_result(unsigned long long* R, bool vec, uint32_t lane, uint64_t tol,
+                                           uint64_t ftol, uint64_t bw, uint64_t fbw, uint64_t nf, uint64_t mab,
+                                           uint64_t mre) {
+  if (vec) {
+    const uint64_t cnt = lane == 0 ? tol : lane == 1 ? bw : nf;
+    if (lane < 3u && cnt != 0) atomicAdd(R + 2 * lane, cnt);
+    const uint64_t first = lane == 0 ? ftol : fbw;
+    if (lane < 2u && first != ~0ull) atomicMin(R + 1 + 2 * lane, first);
+    const uint64_t mx = lane == 0 ? mab : mre;
+    if (lane < 2u && mx != 0) atomicMax(R + 5 + lane, mx);
+  } else if (lane == 0) {
+    if (bw) {
+      atomicAdd(R + 2, bw);
+      atomicMin(R + 3, fbw);
+    }
+    if (tol) {
+      atomicAdd(R + 0, tol);
+      atomicMin(R + 1, ftol);
+    }
+    if (nf) atomicAdd(R + 4, nf);
+    if (mab) atomicMax(R + 5, mab);
+    if (mre) atomicMax(R + 6, mre);
+  }
+}
+
+template <bool VEC>
 __device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment_result* results,
                                       uint32_t lane, uint32_t& nonfinite,
                                       unsigned long long* nonfinite_pairs) {
@@ -1082,25 +1117,60 @@ __device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment
   uint64_t ftol = wave_min(acc.first_tol);
   const uint64_t mab = wave_max(acc.max_abs);
   const uint64_t mre = wave_max(acc.max_rel);
-  if (lane == 0) {
-    asmevo_segment_result* R = results + S.result_index;
-    if (S.mode != ASMEVO_TOLERANCE) {
-      tol = bw;
-      ftol = fbw;
-    }
-    if (bw) {
-      atomicAdd(reinterpret_cast<unsigned long long*>(&R->bitwise_mismatches), bw);
-      atomicMin(reinterpret_cast<unsigned long long*>(&R->first_bitwise), fbw);
-    }
-    if (tol) {
-      atomicAdd(reinterpret_cast<unsigned long long*>(&R->mismatches), tol);
-      atomicMin(reinterpret_cast<unsigned long long*>(&R->first_mismatch), ftol);
-    }
-    if (nf) atomicAdd(reinterpret_cast<unsigned long long*>(&R->nonfinite_mismatches), nf);
-    if (mab) atomicMax(reinterpret_cast<unsigned long long*>(&R->max_abs), mab);
-    if (mre) atomicMax(reinterpret_cast<unsigned long long*>(&R->max_rel), mre);
+  if (S.mode != ASMEVO_TOLERANCE) {
+    tol = bw;
+    ftol = fbw;
   }
+  add_result(reinterpret_cast<unsigned long long*>(results + S.result_index), VEC, lane, tol, ftol, bw, fbw, nf,
+             mab, mre);
   acc_reset(acc);
+}
+
+// The workgroup's last flushes, merged: every wave leaves its partials for
+// its range's last segment (result index `last`, or -1) in LDS; the first
+// wave holding a result adds in the other waves' partials for the same
+// result and flushes them with one set of atomics.  Every wave of the
+// workgroup must call this.
+__device__ __forceinline__ void merge_last(Acc& acc, int last, uint32_t mode, asmevo_segment_result* results,
+                                           uint32_t lane) {
+  constexpr int kW = kDiffBlock / kWave;
+  __shared__ uint64_t fin[kW][8];
+  const uint32_t w = threadIdx.x / kWave;
+  const bool any = last >= 0 && __ballot((acc.bw | acc.tol) != 0u) != 0ull;
+  uint64_t bw = wave_sum(acc.bw), tol = wave_sum(acc.tol), nf = wave_sum(acc.nf);
+  uint64_t fbw = wave_min(acc.first_bw), ftol = wave_min(acc.first_tol);
+  uint64_t mab = wave_max(acc.max_abs), mre = wave_max(acc.max_rel);
+  if (mode != ASMEVO_TOLERANCE) {
+    tol = bw;
+    ftol = fbw;
+  }
+  if (lane == 0) {
+    fin[w][0] = any ? (uint64_t)last : ~0ull;
+    fin[w][1] = tol;
+    fin[w][2] = ftol;
+    fin[w][3] = bw;
+    fin[w][4] = fbw;
+    fin[w][5] = nf;
+    fin[w][6] = mab;
+    fin[w][7] = mre;
+  }
+  __syncthreads();
+  const uint64_t r = fin[w][0];
+  bool first_holder = r != ~0ull;
+  for (uint32_t k = 0; k < w; ++k) first_holder = first_holder && fin[k][0] != r;
+  if (first_holder) {
+    for (uint32_t k = w + 1; k < (uint32_t)kW; ++k) {
+      if (fin[k][0] != r) continue;
+      tol += fin[k][1];
+      ftol = fin[k][2] < ftol ? fin[k][2] : ftol;
+      bw += fin[k][3];
+      fbw = fin[k][4] < fbw ? fin[k][4] : fbw;
+      nf += fin[k][5];
+      mab = fin[k][6] > mab ? fin[k][6] : mab;
+      mre = fin[k][7] > mre ? fin[k][7] : mre;
+    }
+    add_result(reinterpret_cast<unsigned long long*>(results + r), true, lane, tol, ftol, bw, fbw, nf, mab, mre);
+  }
 }
 
 __global__ void diff_init_kernel(asmevo_segment_result* results, int n,
@@ -1150,6 +1220,12 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
   Acc acc;
   acc_reset(acc);
   uint32_t nonfinite = 0;
+  // each wave's last segment is flushed together with the workgroup's other
+  // waves (contiguous ranges only: the waves of a workgroup then end in the
+  // same or neighbouring segments)
+  constexpr bool kMergeLast = kDeal == 0 && kStep == 1 && !COS && !ND;
+  int last = -1;
+  uint32_t last_mode = 0;
   for (uint64_t j = group;; j += ngroups) {
     uint64_t lo, hi;
     if constexpr (kDeal == 0) {
@@ -1188,11 +1264,17 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
         case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
         default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
       }
-      flush(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
+      if (kMergeLast && t_end == hi) {
+        last = (int)S.result_index;    // the range's last segment: merged with the workgroup's below
+        last_mode = S.mode;
+      } else {
+        flush<!ND>(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
+      }
       t += (t_end - t + kStep - 1) / kStep * kStep;   // this wave's first tile at or after t_end
     }
     if constexpr (kDeal == 0) break;
   }
+  if constexpr (kMergeLast) merge_last(acc, last, last_mode, results, lane);
 }
 
 // One level of the cosine's block tree: every workgroup reduces full aligned
