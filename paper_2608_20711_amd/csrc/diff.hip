@@ -1100,15 +1100,21 @@ __device__ __forceinline__ void add_result(unsigned long long* R, bool vec, uint
   }
 }
 
-template <bool VEC>
-__device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment_result* results,
-                                      uint32_t lane, uint32_t& nonfinite,
-                                      unsigned long long* nonfinite_pairs) {
+// The cosine variants' count of pairs with a NaN or Inf, added to S's.
+__device__ __forceinline__ void flush_nonfinite(const DiffSeg& S, uint32_t lane, uint32_t& nonfinite,
+                                                unsigned long long* nonfinite_pairs) {
   if (nonfinite_pairs != nullptr && __ballot(nonfinite != 0u) != 0ull) {
     const uint64_t nfp = wave_sum(nonfinite);
     if (lane == 0) atomicAdd(nonfinite_pairs + S.result_index, (unsigned long long)nfp);
     nonfinite = 0;
   }
+}
+
+template <bool VEC>
+__device__ __forceinline__ void flush(Acc& acc, const DiffSeg& S, asmevo_segment_result* results,
+                                      uint32_t lane, uint32_t& nonfinite,
+                                      unsigned long long* nonfinite_pairs) {
+  flush_nonfinite(S, lane, nonfinite, nonfinite_pairs);
   if (__ballot((acc.bw | acc.tol) != 0u) == 0ull) return;
   uint64_t bw = wave_sum(acc.bw);
   uint64_t tol = wave_sum(acc.tol);
@@ -1221,9 +1227,9 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
   acc_reset(acc);
   uint32_t nonfinite = 0;
   // each wave's last segment is flushed together with the workgroup's other
-  // waves (contiguous ranges only: the waves of a workgroup then end in the
-  // same or neighbouring segments)
-  constexpr bool kMergeLast = kDeal == 0 && kStep == 1 && !COS && !ND;
+  // waves (the 2-D kernels: a workgroup's waves take neighbouring ranges, or
+  // share their blocks, so they end in the same or neighbouring segments)
+  constexpr bool kMergeLast = !ND;
   int last = -1;
   uint32_t last_mode = 0;
   for (uint64_t j = group;; j += ngroups) {
@@ -1264,8 +1270,11 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
         case ASMEVO_I64: diff_range<ASMEVO_I64, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
         default: diff_range<ASMEVO_U8, COS, ND>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot); break;
       }
-      if (kMergeLast && t_end == hi) {
-        last = (int)S.result_index;    // the range's last segment: merged with the workgroup's below
+      // the wave's last segment: its range's (or last block's) end
+      const bool final_seg = t_end == hi && (kDeal == 0 || (j + ngroups) * block >= total_tiles);
+      if (kMergeLast && final_seg) {
+        flush_nonfinite(S, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
+        last = (int)S.result_index;    // merged with the workgroup's other waves below
         last_mode = S.mode;
       } else {
         flush<!ND>(acc, S, results, lane, nonfinite, COS ? nonfinite_pairs : nullptr);
