@@ -475,7 +475,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
     std::reverse(m, m + nm);   // outermost first
     if (nm == 0) m[nm++] = Dim{1, 1, 1, 1};
     const Dim inner = m[nm - 1];
-    const bool unit = inner.sa == 1 && inner.sb == 1;
+    bool unit = inner.sa == 1 && inner.sb == 1;
     X.in_sa = (uint64_t)inner.sa * es;
     X.in_sb = (uint64_t)inner.sb * es;
     X.nouter = (uint32_t)(nm - 1);
@@ -501,9 +501,36 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
       pitches16a = pitches16a && X.opa[d] % 16 == 0;
       pitches16b = pitches16b && X.opb[d] % 16 == 0;
     }
+    // A gather whose elements are s apart in both operands, s * esize <= 64 bytes, rows 16-byte
+    // aligned (the plain diff only: the cosine's order follows the logical elements): its rows are
+    // read as their covering bytes, whole 16-byte chunks like a contiguous row, and only the
+    // elements at multiples of s compare.  The walk then counts covering positions: a last
+    // dimension of s positions with logical pitch 0 maps a position back to its element.  (A
+    // 64-byte memory sector holds at least one element, so the covering bytes are what the
+    // element loads fetch anyway.)
+    const uint64_t s_el = (uint64_t)inner.sa;
+    const bool span = !row_tiled && !unit && inner.sa == inner.sb && inner.sa >= 2 && s_el * es <= 64 &&
+                      S.a % 16 == 0 && S.b % 16 == 0 && pitches16a && pitches16b && nd < ASMEVO_MAX_DIMS;
+    if (span) {
+      X.ishape[nd] = s_el;
+      X.lpitch[nd] = 0;
+      X.ni = (uint32_t)nd + 1;
+      X.in_sa = X.in_sb = (uint64_t)es;
+      D.cols = inner.n * s_el;
+      D.row_bytes = ((inner.n - 1) * s_el + 1) * es;
+      D.row_chunks = (D.row_bytes + kChunk - 1) / kChunk;
+      D.full_chunks = D.row_bytes / kChunk;
+      uint32_t pattern = 0;
+      for (uint32_t k = 0; k < 16; k += (uint32_t)s_el) pattern |= 1u << k;
+      D.span = (uint32_t)s_el | (pattern << 8);
+      permuted = true;
+      unit = true;
+    }
+    const bool narrow_s = !row_tiled && D.rows > 1 && D.row_chunks < (uint64_t)kTileChunks / 2;
     const bool pair2a = !unit && inner.sa == 2 && S.a % 16 == 0 && pitches16a;
     const bool pair2b = !unit && inner.sb == 2 && S.b % 16 == 0 && pitches16b;
-    D.flags = (aligned ? kSegVec : 0u) | (narrow ? kSegNarrow : 0u) | (unit ? 0u : kSegGather) |
+    D.flags = ((aligned || span) ? kSegVec : 0u) | ((span ? narrow_s : narrow) ? kSegNarrow : 0u) |
+              (unit ? 0u : kSegGather) | (span ? kSegSpan : 0u) |
               (pair2a ? kSegPair2A : 0u) | (pair2b ? kSegPair2B : 0u) |
               (permuted ? kSegPermuted : 0u) |
               ((S.mode == ASMEVO_TOLERANCE && S.nan_policy == ASMEVO_NAN_STRICT) ? kSegStrict : 0u);
@@ -511,7 +538,7 @@ asmevo_status plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int32_t n_r
       D.nd_ext = n_ext++;
       ext.push_back(X);
     }
-    if (narrow) {
+    if (D.flags & kSegNarrow) {
       D.tile_count = (D.rows * D.row_chunks + kTileChunks - 1) / kTileChunks;
     } else {
       const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;

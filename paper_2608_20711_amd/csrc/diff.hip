@@ -454,6 +454,45 @@ __device__ __forceinline__ void load_nd_chunk(const uint8_t* pa, const uint8_t* 
   }
 }
 
+// A span row (kSegSpan): chunk c of the row's covering bytes keeps the
+// elements at row positions that are multiples of s (bits 0-7 of `span`) and
+// masks the others to zero, the same on both operands, so they compare equal
+// on every path.  `r` is (c * elements per chunk) mod s; bits 8-23 of `span`
+// hold the positions k < 16 with k mod s == 0.
+template <int DT>
+__device__ __forceinline__ void span_mask(uint32_t span, uint32_t r, u32x4& va, u32x4& vb) {
+  constexpr uint32_t es = Et<DT>::es, epc = 16 / es;
+  const uint32_t s = span & 0xFFu;
+  const uint32_t t = r == 0 ? 0u : s - r;                      // first kept position in the chunk
+  const uint32_t bits = t < epc ? ((span >> 8) << t) & ((1u << epc) - 1u) : 0u;
+  u32x4 m;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint32_t w;
+    if constexpr (es == 8) {
+      w = (bits >> (k >> 1)) & 1u ? ~0u : 0u;
+    } else if constexpr (es == 4) {
+      w = (bits >> k) & 1u ? ~0u : 0u;
+    } else if constexpr (es == 2) {
+      w = ((bits >> (2 * k)) & 1u ? 0x0000FFFFu : 0u) | ((bits >> (2 * k + 1)) & 1u ? 0xFFFF0000u : 0u);
+    } else {
+      const uint32_t x = (bits >> (4 * k)) & 0xFu;             // four bits to the low bits of four bytes
+      w = ((x * 0x00204081u) & 0x01010101u) * 0xFFu;
+    }
+    m[k] = w;
+  }
+  va &= m;
+  vb &= m;
+}
+
+// (c * elements per chunk) mod s for chunk c of a span row.
+template <int DT>
+__device__ __forceinline__ uint32_t span_residue(uint64_t c, uint32_t span) {
+  const uint64_t s = span & 0xFFu;
+  const uint64_t p = c * (uint64_t)(16 / Et<DT>::es);
+  return (uint32_t)(((p >> 32) == 0) ? (uint32_t)p % (uint32_t)s : p % s);
+}
+
 // n / d and n % d, in 32 bits when both fit.
 __device__ __forceinline__ void divmod(uint64_t n, uint64_t d, uint64_t& q, uint64_t& r) {
   if (((n | d) >> 32) == 0) {
@@ -757,6 +796,8 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
   uint64_t ibase0 = 0, in_sa = 0, in_sb = 0;
   bool gather = false, permuted = false, pair2a = false, pair2b = false;
+  uint32_t span = 0;                      // a span row's stride and pattern (the plain N-D diff)
+  if constexpr (ND && !COS) span = (S.flags & kSegSpan) ? S.span : 0u;
   if constexpr (ND) {
     permuted = (S.flags & kSegPermuted) != 0;
     ibase0 = permuted ? 0 : S.nd_index_base;  // reordered: indices are mapped on a mismatch
@@ -808,6 +849,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
             if (S.rows > 1) nd_row_offsets(X, r, oa, ob);   // a segment of several rows has an extension
             load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb[j], vec, gather, in_sa, in_sb, pair2a, pair2b,
                               c + 1 == S.row_chunks, va[j], vb[j]);
+            if (span) span_mask<DT>(span, span_residue<DT>(c, span), va[j], vb[j]);
           } else {
             load_chunk<DT>(a0 + r * S.a_pitch + cb, b0 + r * S.b_pitch + cb, nb[j], vec, va[j], vb[j]);
           }
@@ -887,6 +929,18 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           va[j] = ld_nt(qa + j * kWave * kChunk);
           vb[j] = ld_nt(qb + j * kWave * kChunk);
           nv[j] = epc;
+        }
+        if (span) {
+          // a lane's chunks are 64 apart: the residue steps by (64 * elements per chunk) mod s
+          const uint32_t sp = span & 0xFFu;
+          const uint32_t step_r = (uint32_t)(kWave * epc) % sp;
+          uint32_t r = span_residue<DT>(k0 + lane, span);
+#pragma unroll
+          for (int j = 0; j < U; ++j) {
+            span_mask<DT>(span, r, va[j], vb[j]);
+            r += step_r;
+            r = r >= sp ? r - sp : r;
+          }
         }
       }
       u32x4 x = va[0] ^ vb[0];
@@ -1005,10 +1059,13 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
           const uint64_t cb = c * kChunk;
           const uint64_t rem = S.row_bytes - cb;
           nb[j] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-          if constexpr (ND)
+          if constexpr (ND) {
             load_nd_chunk<DT>(pa, pb, c, nb[j], vec, gather, in_sa, in_sb, pair2a, pair2b,
                               c + 1 == S.row_chunks, va[j], vb[j]);
-          else load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
+            if (span) span_mask<DT>(span, span_residue<DT>(c, span), va[j], vb[j]);
+          } else {
+            load_chunk<DT>(pa + cb, pb + cb, nb[j], vec, va[j], vb[j]);
+          }
         }
       }
       uint64_t i0[U];

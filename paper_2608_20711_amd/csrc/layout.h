@@ -45,6 +45,8 @@ enum : uint32_t {
   kSegPermuted = 32u, // N-D: visited in memory order, not logical order (see NdExt)
   kSegPair2A = 64u,   // N-D gather: a's elements are 2 apart and its rows start 16-byte aligned
   kSegPair2B = 128u,  // ... the same for b
+  kSegSpan = 256u,    // N-D: a gather read as its rows' covering bytes; only the elements at
+                      // multiples of `span` compare (the others are masked to zero on both sides)
 };
 
 // A segment is either "row-tiled" (every tile lies inside one row: contiguous
@@ -69,7 +71,12 @@ struct DiffSeg {                // 128 bytes
   uint64_t tile_count;
   double atol, rtol;
   uint32_t dtype, mode, flags, esize;
-  uint32_t result_index, tiles_per_row;
+  uint32_t result_index;
+  union {
+    uint32_t tiles_per_row;     // 2-D: tiles of one row
+    uint32_t span;              // N-D: 0, or a span row (kSegSpan): bits 0-7 the element
+                                // stride s, bits 8-23 bit k set iff k mod s == 0 (k < 16)
+  };
 };
 static_assert(sizeof(DiffSeg) == 128, "DiffSeg layout");
 

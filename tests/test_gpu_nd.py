@@ -207,6 +207,87 @@ def test_every_other_element_views(dtype):
     assert any(w["mismatches"] for w in want_all)
 
 
+_RAW_T = {"f32": np.float32, "f16": np.float16, "bf16": np.uint16, "fp8e4m3": np.uint8, "i64": np.int64,
+          "u8": np.uint8}
+
+
+def _raw_pair(dtype, n, rng):
+    """A reference buffer of n elements and a candidate that differs from it at
+    about 2 % of the elements, with NaNs for the float types (raw patterns for
+    bf16 and fp8)."""
+    t = _RAW_T[dtype]
+    if dtype in ("f32", "f16"):
+        b = rng.standard_normal(n).astype(t)
+    elif dtype == "bf16":
+        b = (rng.standard_normal(n).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    elif dtype == "fp8e4m3":
+        b = rng.integers(0, 256, size=n, dtype=np.uint8)
+        b[(b & 0x7F) == 0x7F] ^= 1                         # finite reference values
+    else:
+        b = rng.integers(0, 1 << 20, size=n).astype(t)
+    a = b.copy()
+    idx = rng.choice(n, size=max(1, n // 50), replace=False)
+    av = a.view(np.uint8).reshape(n, -1)
+    av[idx, 0] ^= np.uint8(1) << rng.integers(0, 8, size=idx.size).astype(np.uint8)
+    if dtype in ("f32", "f16", "bf16", "fp8e4m3"):
+        nan = {"f32": np.uint32(0x7FC00000), "f16": np.uint16(0x7E00), "bf16": np.uint16(0x7FC0),
+               "fp8e4m3": np.uint8(0x7F)}[dtype]
+        j = rng.choice(n, size=max(1, n // 400), replace=False)
+        a.view(nan.dtype)[j] = nan
+        b.view(nan.dtype)[j[: j.size // 2]] = nan          # half of them on both sides
+    return b, a
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16", "fp8e4m3", "i64", "u8"])
+def test_strided_views_read_as_spans(dtype):
+    """Gathers whose elements are s apart in both operands, s * esize up to 64
+    bytes: with 16-byte aligned rows the plain N-D diff reads each row's
+    covering bytes and compares only the elements at multiples of s.  The
+    bytes between those elements differ between the operands (and hold NaN
+    patterns) and must not count.  One long row, long rows spanning tiles,
+    short rows (the narrow walk), a start off the 16-byte grid (the
+    element-by-element path), ragged ends and a broadcast dimension; both NaN
+    policies, index bases."""
+    rng = np.random.default_rng(21)
+    es = np.dtype(_RAW_T[dtype]).itemsize
+    strides = sorted({2, 3, 4, 5, 8, 16, 64 // es} & set(range(2, 64 // es + 1)))
+    specs_all, got_all, want_all = [], [], []
+    for s_el in strides:
+        n = 64 * 1024 // es * 3 + 37                        # not a whole number of rows or chunks
+        b, a = _raw_pair(dtype, n, rng)
+        row_long = 4096 // es * 4                           # elements per long row (16 KiB)
+        row_short = 256 // es                               # 256 bytes: a few chunks per row
+        g = 16 // es                                        # elements per 16 bytes
+        views = [
+            lambda x: x[::s_el],                                              # one long row
+            lambda x: x[: x.size - 5][::s_el],                                # a ragged end
+            lambda x: x[g:][::s_el],                                          # starts 16 bytes in
+            lambda x: x[1:][::s_el] if es < 16 else x[::s_el],                # off the grid: elementwise
+            lambda x: x[: (x.size // row_long) * row_long].reshape(-1, row_long)[:, ::s_el],
+            lambda x: x[: (x.size // row_short) * row_short].reshape(-1, row_short)[:, ::s_el],
+            lambda x: x[: (x.size // row_short) * row_short].reshape(-1, row_short)[3:40, g::s_el],
+            lambda x: np.broadcast_to(x[: row_long * 2].reshape(2, row_long)[:1, ::s_el],
+                                      (3, (row_long + s_el - 1) // s_el)),
+        ]
+        specs = []
+        for k, v in enumerate(views):
+            for policy in (("equal", "strict") if dtype in ("f32", "f16", "bf16", "fp8e4m3") else ("equal",)):
+                sp = _spec(v(a), a, b, dtype, policy=policy, result=len(specs), index_base=1000 * k + 3,
+                           view_b=v(b))
+                if dtype in ("bf16", "fp8e4m3"):
+                    sp["mode"] = "tolerance"
+                specs.append(sp)
+        got, want = _run(specs, a, b)
+        specs_all += specs
+        got_all += got
+        want_all += want
+        # the bytes between the elements differ: a plain contiguous compare of the covering region
+        # would count them, the strided view must not
+        assert any(w["bitwise_mismatches"] for w in want)
+    assert_results_equal(got_all, want_all, f"{dtype} strided views")
+    log(f"strided {dtype}: strides {strides}, {len(specs_all)} views equal")
+
+
 # ------------------------------------------------------------ the cosine term over N-D segments
 def _run_cos(specs, a_host: np.ndarray, b_host: np.ndarray, n_results: int):
     """asmevo_diff_cosine_nd over specs (the segments of a result consecutive):
