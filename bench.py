@@ -75,8 +75,8 @@ def parse():
                         "(host planning and descriptor upload per check) and report it beside the metric")
     p.add_argument("--nd-steps", type=int, default=3,
                    help="after the timed steps, time N-D views of the two states (sliced rows, a "
-                        "permuted 4-D layout, a transposed matrix, a stride-2 gather, narrow half rows, "
-                        "a block table)")
+                        "permuted 4-D layout, a transposed matrix, stride-2 and stride-3 gathers, every "
+                        "8th byte, narrow half rows, a block table)")
     p.add_argument("--read-probe", type=int, default=-1, metavar="GIB",
                    help="after the timed steps, run the two-stream HBM read probe over GIB per "
                         "side and report it as the measured read ceiling (-1: the workload's "
@@ -183,6 +183,8 @@ def nd_cases(st, stream, steps: int, scratch):
     if n >= m * 16:
         cases["transposed"] = [([n // m, m], [1, n // m], 0)]
     cases["stride2_gather"] = [([n // 2], [2], 0)]
+    cases["stride3_gather"] = [([n // 3], [3], 0)]
+    cases["stride8_gather_u8"] = [([4 * n // 8], [8], 0, lib.U8)]            # every 8th byte
     cases["half_rows_256B"] = [([n // 128, 64], [128, 1], 0)]      # narrow rows: 256 of every 512 bytes
     blk = 1 << 19                                              # 2 MiB blocks
     if n >= 4 * blk:
@@ -193,11 +195,16 @@ def nd_cases(st, stream, steps: int, scratch):
     for name, parts in cases.items():
         segs = []
         elems = 0
-        for j, (shape, strides, off) in enumerate(parts):
+        es = 4
+        for j, part in enumerate(parts):
+            shape, strides, off = part[:3]
+            dt = part[3] if len(part) > 3 else lib.F32
+            es = 1 if dt == lib.U8 else 4
             cnt = int(np.prod(shape))
-            span = (sum((k - 1) * v for k, v in zip(shape, strides)) + 1) * 4
-            assert off * 4 + span <= st.cand.numel() and off * 4 + span <= st.ref.numel(), name
-            segs.append(lib.segment_nd(A + off * 4, B + off * 4, lib.F32, lib.TOLERANCE, lib.NAN_EQUAL,
+            span = (sum((k - 1) * v for k, v in zip(shape, strides)) + 1) * es
+            assert off * es + span <= st.cand.numel() and off * es + span <= st.ref.numel(), name
+            segs.append(lib.segment_nd(A + off * es, B + off * es, dt,
+                                       lib.BITWISE if dt == lib.U8 else lib.TOLERANCE, lib.NAN_EQUAL,
                                        shape, strides, strides, 0.0, 0.0, 0, elems))
             elems += cnt
         n_segs = len(segs)
@@ -214,9 +221,9 @@ def nd_cases(st, stream, steps: int, scratch):
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1))
         med = statistics.median(times[1:])
-        gbps = 2 * 4 * elems / (med * 1e-3) / 1e9
+        gbps = 2 * es * elems / (med * 1e-3) / 1e9
         out[name] = {"segments": n_segs, "shape": parts[0][0], "strides": parts[0][1],
-                     "logical_bytes_per_side": 4 * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
+                     "logical_bytes_per_side": es * elems, "ms_median": round(med, 4), "GBps": round(gbps, 2),
                      "pct_of_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2)}
         del ws
         # the same check planned once (asmevo_plan_diff_nd): no planning or upload in the span
@@ -234,7 +241,10 @@ def nd_cases(st, stream, steps: int, scratch):
             times.append(e0.elapsed_time(e1))
         out[name]["planned_ms_median"] = round(statistics.median(times[1:]), 4)
         del pws
-        # the same view with the cosine term (asmevo_diff_cosine_nd: row-tiled walk, block trees)
+        # the same view with the cosine term (asmevo_diff_cosine_nd: row-tiled walk, block trees);
+        # float views only
+        if dt == lib.U8:
+            continue
         cws = torch.empty(lib.diff_cosine_nd_workspace_bytes(segs, 1), dtype=torch.uint8, device=st.cand.device)
         cres = torch.empty(64, dtype=torch.uint8, device=st.cand.device)
         times = []
@@ -248,7 +258,7 @@ def nd_cases(st, stream, steps: int, scratch):
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1))
         med = statistics.median(times[1:])
-        out[name]["cosine"] = {"ms_median": round(med, 4), "GBps": round(2 * 4 * elems / (med * 1e-3) / 1e9, 2)}
+        out[name]["cosine"] = {"ms_median": round(med, 4), "GBps": round(2 * es * elems / (med * 1e-3) / 1e9, 2)}
         del cws
     return out
 
