@@ -33,7 +33,8 @@
  * against numpy.isclose; the fill's ln/sin/cos against libm; closed-form
  * counts of constructed cases; brute force over every (index, bit) of tiny
  * buffers and every byte of tiny guards; the exact sums against Python's
- * exact rationals and math.fsum; the region copy against numpy slices.
+ * exact rationals and math.fsum; the region copy against numpy slices; the
+ * per-pair bulk loop against one-element segments and numpy.
  */
 #include "ref_oracle.h"
 
