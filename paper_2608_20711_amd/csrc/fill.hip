@@ -425,9 +425,13 @@ __device__ __forceinline__ void fill_one_chunk(const FillAlloc& A, const FillAll
   }
   if (!done) general_chunk(A, rules, os, seed, w);
   if (os >= 0 && o + 16 <= tot) {             // base + o is 16-byte aligned
+    // Non-temporal: the state is written once and read next by a full pass
+    // over all of it.  With ordinary stores the last ~256 MB written stayed
+    // in the memory-side cache and the diff that followed the fill ran 2 %
+    // slower over the 64 GiB sweep (20.76 against 20.31 ms).
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
     const u32x4 v = {w[0], w[1], w[2], w[3]};
-    *gptr_mut<u32x4>(A.base + o) = v;
+    __builtin_nontemporal_store(v, gptr_mut<u32x4>(A.base + o));
   } else {                                    // only the allocation's own bytes
     for (uint32_t b = 0; b < 16; ++b) {
       const int64_t p = os + (int64_t)b;
