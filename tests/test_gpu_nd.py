@@ -100,6 +100,8 @@ def test_views_of_one_tensor(dtype):
         lambda x: x.transpose(0, 1, 3, 2),                # innermost not unit-stride: gather
         lambda x: x.transpose(3, 2, 1, 0),
         lambda x: x[1:5, ::3, 2:30, 7:45],                # sliced, short rows
+        lambda x: x[:, :, :, 7:45],                       # short rows whose outer dimensions merge into one
+        lambda x: x[:, :, :, 8:40],                       # the same, rows 16-byte aligned for 8-byte elements
         lambda x: x[:, 2:9, :, :],                        # merges to long rows
         lambda x: x[::2, :, 5, :],                        # a dropped dimension
         lambda x: x[0, 0, 0, 0:1],                        # one element
