@@ -680,10 +680,8 @@ __device__ __forceinline__ double f64_of(uint32_t hi, uint32_t lo) {
 // 32 bits at a time: row_ror:R (0x120 + R) gives lane i of each 16-lane row
 // the value of lane (i + 16 - R) mod 16; quad_perm 0x4E and 0xB1 give lane i
 // of each group of four the value of lane i ^ 2 and i ^ 1.  Every lane has a
-// source under these patterns, so no old value is merged in: without one the
-// compiler no longer zeroes a register before each move (24 VALU instructions
-// fewer per block record, and the cosine pass over the 64 GiB sweep 0.1 ms
-// faster).
+// source under these patterns, so no old value is merged in, and the
+// compiler zeroes no register before each move.
 template <int CTRL>
 __device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t u = (uint64_t)__double_as_longlong(v);
