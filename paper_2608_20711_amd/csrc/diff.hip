@@ -528,8 +528,9 @@ __device__ __forceinline__ void nd_row_offsets(const NdExt* X, uint64_t r, uint6
 // null), read once per range.  The short-row paths find the row of every
 // chunk, and reading the extension there cost each wave-load three more
 // vector loads: a view of 256-byte rows over 2 x 8 GiB took 3.12 ms against
-// 2.64 ms with this.  With one outer dimension (a matrix, or dimensions that
-// merged) a row's offsets are one product each.
+// 2.64 ms with this in the plain diff, and 5.90 against 4.96 ms with this and
+// the DPP group fold in the cosine pass.  With one outer dimension (a matrix,
+// or dimensions that merged) a row's offsets are one product each.
 struct NdRows {
   const NdExt* X;
   uint32_t nouter;
@@ -690,6 +691,15 @@ __device__ __forceinline__ double dpp_f64(double v) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// Lanes 0-15 and 32-47 receive v of the lane 16 up (v_permlane16_swap);
+// the other lanes receive anything.
+__device__ __forceinline__ double row_up16(double v) {
+  const uint32_t any = __builtin_nondeterministic_value(0u);
+  const auto lo = __builtin_amdgcn_permlane16_swap(lo32(v), any, false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap(hi32(v), any, false, false);
+  return f64_of(hi[1], lo[1]);
+}
+
 // Folds the lane sums of a block and stores its record out[0..3] =
 // {Σab, Σaa, Σbb, 0}: the xor butterfly's tree, lanes 32 apart first, then 16,
 // 8, 4, 2, 1 (fp64 addition commutes, and the lane sums are finite, so every
@@ -757,6 +767,8 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
   while ((1u << lg) < R) ++lg;
   const uint32_t P = 1u << lg, G = (uint32_t)kWave >> lg;
   const uint32_t g = lane >> lg, t = lane & (P - 1);
+  NdRows walk{};
+  if constexpr (ND) walk = nd_rows(X);     // entered for segments of several rows only
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
   // one chunk pair per lane in flight (registers are short in this variant)
@@ -770,7 +782,7 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
       nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
       if constexpr (ND) {
         uint64_t oa = 0, ob = 0;
-        nd_row_offsets(X, row, oa, ob);
+        row_offsets(walk, row, oa, ob);
         load_nd_chunk<DT>(a0 + oa, b0 + ob, t, nb, vec, gather, in_sa, in_sb, pair2a, pair2b, t + 1 == R, va, vb);
       } else {
         load_chunk<DT>(a0 + row * S.a_pitch + cb, b0 + row * S.b_pitch + cb, nb, vec, va, vb);
@@ -784,10 +796,35 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
       cs = Cos{0.0, 0.0, 0.0};
       cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
     }
-    for (uint32_t m = P >> 1; m >= 1; m >>= 1) {
-      cs.ab = cs.ab + __shfl_xor(cs.ab, (int)m, kWave);
-      cs.aa = cs.aa + __shfl_xor(cs.aa, (int)m, kWave);
-      cs.bb = cs.bb + __shfl_xor(cs.bb, (int)m, kWave);
+    // The butterfly over each group of P lanes; only the group's first lane
+    // (t == 0) keeps its sum, so a step may hand the other lanes anything.
+    // Within 16-lane rows the steps are DPP moves (row_ror:8 is xor 8;
+    // row_ror:12 gives lanes 0-3 of each 8 the value 4 lanes up), across rows
+    // (P = 32) one swap of odd and even rows.
+    if (P == 32) {
+      cs.ab = cs.ab + row_up16(cs.ab);
+      cs.aa = cs.aa + row_up16(cs.aa);
+      cs.bb = cs.bb + row_up16(cs.bb);
+    }
+    if (P >= 16) {
+      cs.ab = cs.ab + dpp_f64<0x128>(cs.ab);
+      cs.aa = cs.aa + dpp_f64<0x128>(cs.aa);
+      cs.bb = cs.bb + dpp_f64<0x128>(cs.bb);
+    }
+    if (P >= 8) {
+      cs.ab = cs.ab + dpp_f64<0x12C>(cs.ab);
+      cs.aa = cs.aa + dpp_f64<0x12C>(cs.aa);
+      cs.bb = cs.bb + dpp_f64<0x12C>(cs.bb);
+    }
+    if (P >= 4) {
+      cs.ab = cs.ab + dpp_f64<0x4E>(cs.ab);
+      cs.aa = cs.aa + dpp_f64<0x4E>(cs.aa);
+      cs.bb = cs.bb + dpp_f64<0x4E>(cs.bb);
+    }
+    if (P >= 2) {
+      cs.ab = cs.ab + dpp_f64<0xB1>(cs.ab);
+      cs.aa = cs.aa + dpp_f64<0xB1>(cs.aa);
+      cs.bb = cs.bb + dpp_f64<0xB1>(cs.bb);
     }
     if (t == 0 && row < t_end) {
       double* rec = partials + kCosRec * (S.tile_begin + row);
