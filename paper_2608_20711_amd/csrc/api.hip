@@ -94,9 +94,41 @@ int device_cus() {
 // full resident set, whose more concurrent read streams cost DRAM locality --
 // and two per CU below 4 GiB of operands, where the second wave per SIMD
 // hides the slow path of states with many differences (decode state +4 %).
-int diff_workgroups(uint64_t tiles) {
+// Workgroups of the plain 2-D diff: one per CU once the operands hold 4 GiB
+// (fewer read streams are faster there), two below, and two whenever short
+// rows (the flattened walk, a division per lane and tile) hold 2 % of the
+// tiles or more: rows of 64 of every 128 fp32 over 2 x 16 GiB took 2.61 ms
+// at two workgroups per CU against 3.66 ms at one.
+int diff_workgroups(const DiffSeg* dev, int32_t n, uint64_t tiles) {
+  uint64_t narrow = 0;
+  for (int32_t k = 0; k < n; ++k)
+    if (dev[k].flags & kSegNarrow) narrow += dev[k].tile_count;
   const uint64_t operand_bytes = tiles * (uint64_t)kTileChunks * kChunk * 2;
-  return device_cus() * (operand_bytes < (4ull << 30) ? 2 : 1);
+  return device_cus() * (operand_bytes < (4ull << 30) || narrow * 50 >= tiles ? 2 : 1);
+}
+
+// Workgroups of the plain N-D diff.  Tiles other than whole 16-byte aligned
+// 4 KiB runs of a row (short rows, the last tile of a row, gathers) cost the
+// kernel more per byte, and more resident waves hide that; whole tiles
+// stream fastest from one workgroup per CU once the operands hold 4 GiB, as
+// in the 2-D diff.  Measured on 2 x 16 GiB views, one workgroup per CU
+// against the resident set: transposed 5.14 against 5.42 ms, a block table
+// of 2 MiB blocks 5.34 against 5.55 ms; 256-byte half rows 6.20 against
+// 2.65 ms, rows of 4032 elements 8.00 against 5.23 ms.
+int nd_workgroups(const std::vector<DiffSeg>& dev, uint64_t tiles) {
+  uint64_t other = 0;
+  for (const DiffSeg& D : dev) {
+    if (D.tile_count == 0) continue;
+    if ((D.flags & kSegNarrow) || !(D.flags & kSegVec) || (D.flags & kSegGather)) {
+      other += D.tile_count;
+      continue;
+    }
+    const uint64_t tpr = (D.row_chunks + kTileChunks - 1) / kTileChunks;
+    other += D.rows * (tpr - D.full_chunks / kTileChunks);
+  }
+  const uint64_t operand_bytes = tiles * (uint64_t)kTileChunks * kChunk * 2;
+  const bool stream = operand_bytes >= (4ull << 30) && other * 50 < tiles;   // under 2 % of the tiles
+  return device_cus() * (stream ? 1 : diff_nd_blocks_per_cu());
 }
 
 template <typename T>
@@ -669,7 +701,7 @@ asmevo_status asmevo_diff_segments_ex(const asmevo_segment* segs, int32_t n,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(hipMemcpyAsync(workspace, dev.data(), bytes, hipMemcpyHostToDevice, s));
   int wg = workgroups;
-  if (wg == 0) wg = diff_workgroups(tiles);
+  if (wg == 0) wg = diff_workgroups(dev.data(), n, tiles);
   HIP_TRY(launch_diff(reinterpret_cast<const DiffSeg*>(workspace), n, tiles, results, wg, s));
   return ASMEVO_OK;
 }
@@ -735,7 +767,7 @@ asmevo_status asmevo_diff_segments_noalloc(const asmevo_segment* segs, int32_t n
   // pageable source: HIP has read it when the call returns, so the host
   // table may be planned again by the next call
   HIP_TRY(hipMemcpyAsync(table, g_noalloc_host, (size_t)n * sizeof(DiffSeg), hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_diff(table, n, tiles, results, diff_workgroups(tiles), s));
+  HIP_TRY(launch_diff(table, n, tiles, results, diff_workgroups(g_noalloc_host, n, tiles), s));
   return ASMEVO_OK;
 }
 
@@ -766,7 +798,7 @@ asmevo_status asmevo_diff_segments_nd(const asmevo_segment_nd* segs, int32_t n,
     put(host, off_ext, ext);
     HIP_TRY(hipMemcpyAsync(ws, host.data(), bytes, hipMemcpyHostToDevice, s));
   }
-  const int wg = device_cus() * diff_nd_blocks_per_cu();
+  const int wg = nd_workgroups(dev, tiles);
   HIP_TRY(launch_diff_nd(reinterpret_cast<const DiffSeg*>(ws), reinterpret_cast<const NdExt*>(ws + off_ext),
                          n, n_results, tiles, results, wg, s));
   return ASMEVO_OK;
@@ -1018,7 +1050,7 @@ asmevo_status asmevo_plan_diff(const asmevo_segment* segs, int32_t n, void* work
   plan->n = n;
   plan->n_results = n;
   plan->kind = ASMEVO_PLAN_DIFF;
-  plan->workgroups = diff_workgroups(tiles);
+  plan->workgroups = diff_workgroups(dev.data(), n, tiles);
   return ASMEVO_OK;
 }
 
@@ -1047,7 +1079,7 @@ asmevo_status asmevo_plan_diff_nd(const asmevo_segment_nd* segs, int32_t n, int3
   plan->n = n;
   plan->n_results = n_results;
   plan->kind = ASMEVO_PLAN_DIFF_ND;
-  plan->workgroups = device_cus() * diff_nd_blocks_per_cu();
+  plan->workgroups = nd_workgroups(dev, tiles);
   return ASMEVO_OK;
 }
 
