@@ -746,12 +746,15 @@ __device__ __forceinline__ void cos_store(const Cos& c, double* out, uint32_t la
 // are placed by the segment's N-D extension X (the 2-D code otherwise).
 // The cosine variant on rows of at most kNarrowCosChunks chunks, each one
 // block (one tile).  Tiling row by row would leave most of a wave idle: a row
-// of R chunks fills lanes 0..R-1 only.  Instead a wave-load holds G = 64 / P
-// rows, P the power of two at or above R, row g in lanes gP..gP+P-1, and the
-// block sums come from an xor butterfly over each group of P lanes.  That is
-// the block sum of the definition: in the 64-lane butterfly of a row's block,
-// the steps m >= P add lanes that hold +0.0 to lanes 0..P-1 (a lane sum is
-// never -0.0), so lane 0 ends with the butterfly over lanes 0..P-1.
+// of R chunks fills lanes 0..R-1 only.  Instead, with N the power of two at or
+// above R, the block sum is an xor butterfly over the row's first N chunks.
+// That is the block sum of the definition: in the 64-lane butterfly of a
+// row's block, the steps m >= N add lanes that hold +0.0 to lanes 0..N-1 (a
+// lane sum is never -0.0), so lane 0 ends with the butterfly over 0..N-1.
+// A row takes P = N / 2 lanes (one lane for a one-chunk row), a wave-load
+// G = 64 / P rows, row g in lanes gP..gP+P-1.  Lane t holds chunks t and
+// t + P: adding their sums is the butterfly's first step (chunk c with
+// c + N / 2) with no data moved, and the other steps go across the P lanes.
 constexpr uint32_t kNarrowCosChunks = 32;
 
 template <int DT, bool ND>
@@ -765,42 +768,72 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
   const uint32_t R = (uint32_t)S.row_chunks;
   uint32_t lg = 0;
   while ((1u << lg) < R) ++lg;
-  const uint32_t P = 1u << lg, G = (uint32_t)kWave >> lg;
-  const uint32_t g = lane >> lg, t = lane & (P - 1);
+  // QMAX chunks a lane at most (four spilled registers and ran slower than
+  // two); a one-chunk row takes Q = 1
+  constexpr uint32_t QMAX = 2;
+  const uint32_t lq = lg < 1u ? lg : 1u;
+  const uint32_t P = 1u << (lg - lq), G = (uint32_t)kWave >> (lg - lq);
+  const uint32_t Q = 1u << lq;
+  const uint32_t g = lane >> (lg - lq), t = lane & (P - 1);
   NdRows walk{};
   if constexpr (ND) walk = nd_rows(X);     // entered for segments of several rows only
   const uint8_t* a0 = reinterpret_cast<const uint8_t*>(S.a);
   const uint8_t* b0 = reinterpret_cast<const uint8_t*>(S.b);
-  // one chunk pair per lane in flight (registers are short in this variant)
   for (uint64_t tile = t_begin; tile < t_end; tile += (uint64_t)step * G) {
     const uint64_t row = tile + (uint64_t)g * step;
-    u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
-    uint32_t nb = 0;
-    if (row < t_end && t < R) {
-      const uint64_t cb = (uint64_t)t * kChunk;
-      const uint64_t rem = S.row_bytes - cb;
-      nb = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
-      if constexpr (ND) {
-        uint64_t oa = 0, ob = 0;
-        row_offsets(walk, row, oa, ob);
-        load_nd_chunk<DT>(a0 + oa, b0 + ob, t, nb, vec, gather, in_sa, in_sb, pair2a, pair2b, t + 1 == R, va, vb);
-      } else {
-        load_chunk<DT>(a0 + row * S.a_pitch + cb, b0 + row * S.b_pitch + cb, nb, vec, va, vb);
+    u32x4 va[QMAX], vb[QMAX];
+    uint32_t nb[QMAX];
+    uint64_t oa = 0, ob = 0;
+    if constexpr (ND) {
+      if (row < t_end) row_offsets(walk, row, oa, ob);
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < QMAX; ++k) {
+      const uint32_t c = t + k * P;
+      va[k] = u32x4{0u, 0u, 0u, 0u};
+      vb[k] = u32x4{0u, 0u, 0u, 0u};
+      nb[k] = 0;
+      if (row < t_end && k < Q && c < R) {
+        const uint64_t cb = (uint64_t)c * kChunk;
+        const uint64_t rem = S.row_bytes - cb;
+        nb[k] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+        if constexpr (ND) {
+          load_nd_chunk<DT>(a0 + oa, b0 + ob, c, nb[k], vec, gather, in_sa, in_sb, pair2a, pair2b, c + 1 == R,
+                            va[k], vb[k]);
+        } else {
+          load_chunk<DT>(a0 + row * S.a_pitch + cb, b0 + row * S.b_pitch + cb, nb[k], vec, va[k], vb[k]);
+        }
       }
     }
-    chunk<DT, ND>(va, vb, ibase0 + row * S.cols + (uint64_t)t * epc, nb / es, tol_mode, strict, S.atol, S.rtol,
-                  acc, X, permuted);
-    Cos cs{0.0, 0.0, 0.0};
-    cos_chunk_fast<DT>(va, vb, cs);
-    if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
-      cs = Cos{0.0, 0.0, 0.0};
-      cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
+    Cos s[QMAX];
+#pragma unroll
+    for (uint32_t k = 0; k < QMAX; ++k) {
+      chunk<DT, ND>(va[k], vb[k], ibase0 + row * S.cols + (uint64_t)(t + k * P) * epc, nb[k] / es, tol_mode,
+                    strict, S.atol, S.rtol, acc, X, permuted);
+      s[k] = Cos{0.0, 0.0, 0.0};
+      cos_chunk_fast<DT>(va[k], vb[k], s[k]);
+      if (!(__builtin_isfinite(s[k].ab) && __builtin_isfinite(s[k].aa) && __builtin_isfinite(s[k].bb))) {
+        s[k] = Cos{0.0, 0.0, 0.0};
+        cos_chunk<DT>(va[k], vb[k], nb[k] / es, s[k], nonfinite);
+      }
     }
-    // The butterfly over each group of P lanes; only the group's first lane
+    // the first step, in the lane (chunk k with k + QMAX / 2)
+#pragma unroll
+    for (uint32_t h = QMAX / 2; h >= 1; h /= 2) {
+#pragma unroll
+      for (uint32_t k = 0; k < h; ++k) {
+        s[k].ab = s[k].ab + s[k + h].ab;
+        s[k].aa = s[k].aa + s[k + h].aa;
+        s[k].bb = s[k].bb + s[k + h].bb;
+      }
+    }
+    Cos cs = s[0];
+    // The other steps over each group of P lanes; only the group's first lane
     // (t == 0) keeps its sum, so a step may hand the other lanes anything.
     // Within 16-lane rows the steps are DPP moves (row_ror:8 is xor 8;
     // row_ror:12 gives lanes 0-3 of each 8 the value 4 lanes up), across rows
-    // (P = 32) one swap of odd and even rows.
+    // (P = 32, only reached by a build with QMAX = 1) one swap of odd and even
+    // rows.
     if (P == 32) {
       cs.ab = cs.ab + row_up16(cs.ab);
       cs.aa = cs.aa + row_up16(cs.aa);
