@@ -185,10 +185,11 @@ def test_cosine_many_small_segments_mixed_dtypes():
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "fp8e4m3"])
 def test_cosine_every_short_row_width(dtype):
     """Rows of 1 to 32 chunks (plus a partial chunk, and aligned or misaligned
-    pitches) pack 64 / P rows per wave-load, P the power of two at or above
-    the row's chunks, with a butterfly over each group of P lanes: the cosine
-    of every such width, with NaN and Inf among the values, against the
-    oracle's 64-lane definition."""
+    pitches) are packed several to a wave-load, a lane holding chunks t and
+    t + P of its row (2P the power of two at or above the row's chunks) and
+    each group of P lanes finishing the butterfly: the cosine of every such
+    width, with NaN and Inf among the values, against the oracle's 64-lane
+    definition."""
     rng = np.random.default_rng(31)
     es = ESIZE[dtype]
     n = (4 << 20) // es

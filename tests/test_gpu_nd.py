@@ -369,6 +369,33 @@ def test_cosine_views_of_one_tensor(dtype):
         assert all(c["blocks"] > 0 for c in cgot[:7])
 
 
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_cosine_every_short_row_width_nd(dtype):
+    """N-D views whose rows span 1 to 32 chunks, each with a partial last
+    chunk, read with unit stride (sliced, rows aligned to 16 bytes or not)
+    and element by element (a stride-3 gather): a lane holds chunks t and
+    t + P of its row, so every width puts the row's last chunk in one of its
+    two slots.  Each view is a result of its own; the cosine against the
+    oracle's exact sums within the order's bound and bit for bit against the
+    order model, the diff results equal."""
+    rng = np.random.default_rng(23)
+    epc = 16 // np.dtype(NP_T[dtype]).itemsize
+    width = 3 * (32 * epc + epc)
+    b = rng.standard_normal((3, 12, width)).astype(NP_T[dtype])
+    a = _perturbed(b, rng, frac=0.003)
+    specs = []
+    for chunks in range(1, 33):
+        cols = (chunks - 1) * epc + max(1, epc // 2 + chunks % (epc // 2))   # the last chunk partial
+        for v in (lambda x, c=cols: x[:, 1:11, epc:epc + c],        # rows 16-byte aligned: vector loads
+                  lambda x, c=cols: x[:, 1:11, 5:5 + c],            # rows off 16 bytes
+                  lambda x, c=cols: x[:, :, 2:2 + 3 * c:3]):
+            specs.append(_spec(v(a), a, b, dtype, result=len(specs), index_base=7 * len(specs), view_b=v(b)))
+    got, want, cgot, cwant = _run_cos(specs, a, b, len(specs))
+    assert_results_equal(got, want, f"{dtype} short-row widths diff")
+    assert_cosine(cgot, *cwant, f"{dtype} short-row widths cosine")
+    assert all(c["blocks"] > 0 for c in cgot)
+
+
 def test_cosine_block_table_and_large_sliced_views():
     """Results made of several consecutive segments (a paged cache: one
     segment per block, one result per sequence), and large sliced and
