@@ -1412,6 +1412,27 @@ void diff_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext
       }
       s = s_lo;
     }
+    if constexpr (kDeal != 0 && ND) {
+      // The group's next block lies ngroups blocks on, past any number of
+      // segments: gallop from the next segment, then bisect (a step at a
+      // time, a wave re-read hundreds of descriptors per block of a block
+      // table).  The 2-D cosine kernel keeps the steps: with the search in
+      // it, its pass over the sweep ran 0.6 % slower.
+      if (t < hi && s + 1 < n && segs[s + 1].tile_begin <= t) {
+        int a = s + 1, d = 1;          // segs[a].tile_begin <= t
+        while (a + d < n && segs[a + d].tile_begin <= t) {
+          a += d;
+          d <<= 1;
+        }
+        int b = a + d < n ? a + d - 1 : n - 1;
+        while (a < b) {
+          const int mid = (a + b + 1) >> 1;
+          if (segs[mid].tile_begin <= t) a = mid;
+          else b = mid - 1;
+        }
+        s = a;
+      }
+    }
     while (t < hi) {
       while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
       const DiffSeg S = segs[s];
