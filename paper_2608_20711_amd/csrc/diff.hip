@@ -1010,7 +1010,36 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       // Whole tile: issue all loads first, then one combined check.
       u32x4 va[U], vb[U];
       uint32_t nv[U];                      // valid elements per chunk
-      if (kCos && !whole) {
+      if (kCos && !whole && ND && S.full_chunks > 0) {
+        // Every lane loads, with no branch around its loads: a chunk past the
+        // row's whole chunks reads the last whole one (which this tile reads
+        // too) and is then cleared, and a partial last chunk is read again
+        // element by element.  (Loads under a branch, into registers zeroed
+        // first, left waits between them in some builds of this kernel.)
+        const uint64_t fc = S.full_chunks;
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+          const uint64_t cc = c < fc ? c : fc - 1;
+          va[j] = ld_nt(pa + cc * kChunk);
+          vb[j] = ld_nt(pb + cc * kChunk);
+        }
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
+          nv[j] = (uint32_t)epc;
+          if (c >= fc) {
+            va[j] = u32x4{0u, 0u, 0u, 0u};
+            vb[j] = u32x4{0u, 0u, 0u, 0u};
+            nv[j] = 0;
+            if (c < S.row_chunks) {            // the partial last chunk
+              const uint32_t nb = (uint32_t)(S.row_bytes - c * kChunk);
+              load_chunk<DT>(pa + c * kChunk, pb + c * kChunk, nb, true, va[j], vb[j]);
+              nv[j] = nb / es;
+            }
+          }
+        }
+      } else if (kCos && !whole) {
 #pragma unroll
         for (int j = 0; j < U; ++j) {
           const uint64_t c = k0 + (uint64_t)(j * kWave) + lane;
@@ -1196,7 +1225,19 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         else load_chunk<DT>(pa + cb, pb + cb, nb, vec, va, vb);
       }
       chunk<DT, ND>(va, vb, ibase + c * epc, nb / es, tol_mode, strict, S.atol, S.rtol, acc, X, permuted);
-      if constexpr (kCos) cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
+      if constexpr (kCos && ND) {
+        // the unchecked sums first (the elements past nb load as zeros), the
+        // checked ones when a NaN or Inf made them non-finite: the same
+        // additions in the same order either way
+        const Cos keep = cs;
+        cos_chunk_fast<DT>(va, vb, cs);
+        if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
+          cs = keep;
+          cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
+        }
+      } else if constexpr (kCos) {
+        cos_chunk<DT>(va, vb, nb / es, cs, nonfinite);
+      }
     }
     if constexpr (kCos) cos_store(cs, partials + kCosRec * (S.tile_begin + tile), lane);
   }
