@@ -424,6 +424,49 @@ def test_cosine_row_tails_nd(dtype):
     assert all(c["blocks"] > 0 for c in cgot)
 
 
+def test_cosine_block_table_at_scale_equals_gathered_copy():
+    """A shuffled block table of 8192 segments (1 GiB per side, 262144
+    tiles): enough tiles that a workgroup of the cosine pass takes a second
+    dealt block of tiles, thousands of segments past its first.  Its diff and
+    cosine results equal, bit for bit, those of the same bytes gathered into
+    one contiguous segment: the block sums and the tree over a result's
+    blocks do not depend on where its segments lie in memory."""
+    from paper_2608_20711_amd.state import COS_RESULT_DTYPE as COS
+    n_blocks, blk = 8192, 32 * 1024                      # fp32 blocks of 128 KiB: 32 tiles each
+    total = n_blocks * blk
+    g = torch.Generator(device="cuda")
+    g.manual_seed(25)
+    b = torch.randn(total, device="cuda", generator=g)
+    a = b.clone()
+    hit = torch.randint(0, total, (total // 5000,), device="cuda", generator=g)
+    a[hit] = a[hit] * 1.001
+    perm = np.random.default_rng(25).permutation(n_blocks)
+    pt = torch.from_numpy(perm).cuda()
+    a2 = a.view(n_blocks, blk).index_select(0, pt).contiguous().view(-1)
+    b2 = b.view(n_blocks, blk).index_select(0, pt).contiguous().view(-1)
+    code = (lib.DTYPE_CODE["f32"], lib.MODE_CODE["tolerance"], lib.NAN_CODE["equal"])
+    table = [lib.segment_nd(a.data_ptr() + int(p) * blk * 4, b.data_ptr() + int(p) * blk * 4, *code, [blk], [1], [1],
+                            1e-4, 1e-4, 0, j * blk) for j, p in enumerate(perm)]
+    whole = [lib.segment_nd(a2.data_ptr(), b2.data_ptr(), *code, [total], [1], [1], 1e-4, 1e-4, 0, 0)]
+    out = []
+    for segs in (table, whole):
+        res = torch.empty(SEG_RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+        cres = torch.empty(COS.itemsize, dtype=torch.uint8, device="cuda")
+        ws_size = lib.diff_cosine_nd_workspace_bytes(segs, 1)
+        ws = torch.empty(ws_size, dtype=torch.uint8, device="cuda")
+        lib.diff_cosine_nd(segs, res.data_ptr(), 1, cres.data_ptr(), ws.data_ptr(), ws_size)
+        torch.cuda.synchronize()
+        out.append((bytes(res.cpu().numpy()), bytes(cres.cpu().numpy())))
+    assert out[0] == out[1]
+    r = out[0][0]
+    got = np.frombuffer(r, dtype=SEG_RESULT_DTYPE)[0]
+    cg = np.frombuffer(out[0][1], dtype=COS)[0]
+    log(f"block table at scale: {int(got['mismatches'])} mismatches, "
+        f"{int(cg['blocks'])} blocks, cosine {float(cg['cosine']):.12f}")
+    assert int(cg["blocks"]) == total * 4 // 4096
+    assert int(got["mismatches"]) > 0
+
+
 def test_cosine_block_table_and_large_sliced_views():
     """Results made of several consecutive segments (a paged cache: one
     segment per block, one result per sequence), and large sliced and
