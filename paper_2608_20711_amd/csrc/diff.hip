@@ -757,7 +757,8 @@ __device__ __forceinline__ void cos_store(const Cos& c, double* out, uint32_t la
 // c + N / 2) with no data moved, and the other steps go across the P lanes.
 constexpr uint32_t kNarrowCosChunks = 32;
 
-template <int DT, bool ND>
+// QMAX: chunks a lane at most (2 or 4).
+template <int DT, bool ND, uint32_t QMAX = 2>
 __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                                    uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
                                                    double* partials, uint32_t& nonfinite, bool tol_mode,
@@ -768,10 +769,11 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
   const uint32_t R = (uint32_t)S.row_chunks;
   uint32_t lg = 0;
   while ((1u << lg) < R) ++lg;
-  // QMAX chunks a lane at most (four spilled registers and ran slower than
-  // two); a one-chunk row takes Q = 1
-  constexpr uint32_t QMAX = 2;
-  const uint32_t lq = lg < 1u ? lg : 1u;
+  // Q = QMAX chunks a lane, fewer for rows of fewer chunks (in diff_kernel
+  // four spilled registers and ran slower than two)
+  static_assert(QMAX == 2 || QMAX == 4, "two or four chunks a lane");
+  constexpr uint32_t QLOG = QMAX == 4 ? 2u : 1u;
+  const uint32_t lq = lg < QLOG ? lg : QLOG;
   const uint32_t P = 1u << (lg - lq), G = (uint32_t)kWave >> (lg - lq);
   const uint32_t Q = 1u << lq;
   const uint32_t g = lane >> (lg - lq), t = lane & (P - 1);
@@ -817,7 +819,7 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
         cos_chunk<DT>(va[k], vb[k], nb[k] / es, s[k], nonfinite);
       }
     }
-    // the first step, in the lane (chunk k with k + QMAX / 2)
+    // the first steps, in the lane (chunk k with k + QMAX / 2, then with k + 1)
 #pragma unroll
     for (uint32_t h = QMAX / 2; h >= 1; h /= 2) {
 #pragma unroll
@@ -1670,6 +1672,93 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
   out[S.result_index] = r;
 }
 
+
+// The cosine pass over N-D segments whose rows are all short and of a float
+// type (at least two rows of at most kNarrowCosChunks chunks each), for calls
+// made only of such segments: the dealing and the segment search of
+// diff_kernel<true, true>, every range taken by the short-row path.  Without
+// the other paths it needs 125 VGPRs, four waves per SIMD instead of three
+// (256-byte half rows: 3.99 against 4.27 ms; four chunks a lane ran slower,
+// 4.70 ms spilling at three waves per SIMD and 4.44 ms at two).
+template <int DT>
+__device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* X, uint64_t b, uint64_t e,
+                                                 uint32_t step, uint32_t lane, Acc& acc, double* partials,
+                                                 uint32_t& nonfinite) {
+  const bool permuted = (S.flags & kSegPermuted) != 0;
+  diff_range_narrow_cos<DT, true, 2>(S, X, b, e, step, lane, acc, partials, nonfinite, S.mode == ASMEVO_TOLERANCE,
+                                     (S.flags & kSegStrict) != 0, (S.flags & kSegVec) != 0,
+                                     (S.flags & kSegGather) != 0, (S.flags & kSegPair2A) != 0,
+                                     (S.flags & kSegPair2B) != 0, X ? X->in_sa : 0, X ? X->in_sb : 0,
+                                     permuted ? 0 : S.nd_index_base, permuted);
+}
+
+__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(4)))
+void narrow_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
+                       uint64_t total_tiles, asmevo_segment_result* results, double* partials,
+                       unsigned long long* nonfinite_pairs) {
+  constexpr uint32_t kStep = ASMEVO_COS_WAVE_STEP;
+  constexpr uint64_t kDeal = ASMEVO_COS_DEAL;
+  static_assert(kDeal > 0 && (kDiffBlock / kWave) % kStep == 0, "blocks dealt inside a workgroup");
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint64_t wave = (uint64_t)blockIdx.x * (kDiffBlock / kWave) +
+                        __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint64_t ngroups = (uint64_t)gridDim.x * (kDiffBlock / kWave) / kStep;
+  const uint64_t group = wave / kStep;
+  const uint64_t per_group = (total_tiles + ngroups - 1) / ngroups;
+  const uint64_t block = kDeal < per_group ? kDeal : per_group;
+  int s = -1;
+  Acc acc;
+  acc_reset(acc);
+  uint32_t nonfinite = 0;
+  for (uint64_t j = group;; j += ngroups) {
+    const uint64_t lo = j * block;
+    if (lo >= total_tiles) break;
+    const uint64_t hi = lo + block < total_tiles ? lo + block : total_tiles;
+    uint64_t t = lo + wave % kStep;
+    if (t < hi && s < 0) {
+      int s_lo = 0, s_hi = n - 1;        // last segment with tile_begin <= t
+      while (s_lo < s_hi) {
+        const int mid = (s_lo + s_hi + 1) >> 1;
+        if (segs[mid].tile_begin <= t) s_lo = mid;
+        else s_hi = mid - 1;
+      }
+      s = s_lo;
+    }
+    if (t < hi && s + 1 < n && segs[s + 1].tile_begin <= t) {
+      int a = s + 1, d = 1;              // gallop, then bisect, as in diff_kernel
+      while (a + d < n && segs[a + d].tile_begin <= t) {
+        a += d;
+        d <<= 1;
+      }
+      int z = a + d < n ? a + d - 1 : n - 1;
+      while (a < z) {
+        const int mid = (a + z + 1) >> 1;
+        if (segs[mid].tile_begin <= t) a = mid;
+        else z = mid - 1;
+      }
+      s = a;
+    }
+    while (t < hi) {
+      while (s + 1 < n && segs[s + 1].tile_begin <= t) ++s;
+      const DiffSeg S = segs[s];
+      const uint64_t seg_end = S.tile_begin + S.tile_count;
+      const uint64_t t_end = seg_end < hi ? seg_end : hi;
+      const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
+      const NdExt* X = S.nd_ext != ~0ull ? ext + S.nd_ext : nullptr;
+      switch (S.dtype) {
+        case ASMEVO_F32: narrow_cos_range<ASMEVO_F32>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_BF16: narrow_cos_range<ASMEVO_BF16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_F16: narrow_cos_range<ASMEVO_F16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+        case ASMEVO_FP8_E4M3:
+          narrow_cos_range<ASMEVO_FP8_E4M3>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
+          break;
+        default: break;                  // not launched for other types
+      }
+      flush<false>(acc, S, results, lane, nonfinite, nonfinite_pairs);
+      t += (t_end - t + kStep - 1) / kStep * kStep;   // this wave's first tile at or after t_end
+    }
+  }
+}
 }  // namespace
 
 // Resident workgroups per CU of a diff kernel (one code object: queried once).
@@ -1690,6 +1779,29 @@ int cos_blocks_per_cu() { return resident_blocks<true, false>(); }
 int diff_nd_blocks_per_cu() { return resident_blocks<false, true>(); }
 
 int cos_nd_blocks_per_cu() { return resident_blocks<true, true>(); }
+
+int narrow_cos_blocks_per_cu() {
+  static const int blocks = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, narrow_cos_kernel, kDiffBlock, 0) != hipSuccess || b <= 0)
+      b = 3;
+    return b;
+  }();
+  return blocks;
+}
+
+bool cos_nd_short_rows_only(const DiffSeg* segs, int n) {
+  bool any = false;
+  for (int k = 0; k < n; ++k) {
+    const DiffSeg& S = segs[k];
+    if (S.tile_count == 0) continue;
+    const bool fp = S.dtype == ASMEVO_F32 || S.dtype == ASMEVO_BF16 || S.dtype == ASMEVO_F16 ||
+                    S.dtype == ASMEVO_FP8_E4M3;
+    if (!fp || S.rows < 2 || S.row_chunks > (uint64_t)kNarrowCosChunks) return false;
+    any = true;
+  }
+  return any;
+}
 
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
                        asmevo_segment_result* results, int workgroups, hipStream_t stream,
@@ -1753,7 +1865,7 @@ hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, c
                                  int workgroups, hipStream_t stream, double* partials,
                                  unsigned long long* nonfinite_pairs, asmevo_cosine_result* cos_results,
                                  const CosLevels* levels_of, const uint64_t* level_prefix,
-                                 const uint64_t* level_groups, double* levels) {
+                                 const uint64_t* level_groups, double* levels, bool short_rows) {
   if (n_results == 0) return hipSuccess;
   hipLaunchKernelGGL(diff_init_kernel, dim3((n_results + 255) / 256), dim3(256), 0, stream, results, n_results,
                      nonfinite_pairs);
@@ -1762,8 +1874,12 @@ hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, c
   if (n > 0 && total_tiles > 0) {
     const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
     const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
-    hipLaunchKernelGGL((diff_kernel<true, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
-                       total_tiles, results, partials, nonfinite_pairs);
+    if (short_rows)
+      hipLaunchKernelGGL(narrow_cos_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n, total_tiles,
+                         results, partials, nonfinite_pairs);
+    else
+      hipLaunchKernelGGL((diff_kernel<true, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
+                         total_tiles, results, partials, nonfinite_pairs);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
