@@ -875,8 +875,8 @@ asmevo_status asmevo_diff_cosine_nd(const asmevo_segment_nd* segs, int32_t n, as
     put(host, P.off_ext - P.off_segs, P.ext);
     HIP_TRY(hipMemcpyAsync(ws + P.off_segs, host.data(), host.size(), hipMemcpyHostToDevice, s));
   }
-  const bool short_rows = cos_nd_short_rows_only(P.dev.data(), (int)P.dev.size());
-  const int wg = device_cus() * (short_rows ? narrow_cos_blocks_per_cu() : cos_nd_blocks_per_cu());  // resident
+  const int variant = cos_nd_variant(P.dev.data(), (int)P.dev.size());
+  const int wg = device_cus() * (variant == kCosNdMixed ? cos_nd_blocks_per_cu() : split_cos_blocks_per_cu(variant));
   HIP_TRY(launch_diff_cosine_nd(reinterpret_cast<const DiffSeg*>(ws + P.off_segs),
                                 reinterpret_cast<const NdExt*>(ws + P.off_ext), n,
                                 reinterpret_cast<const DiffSeg*>(ws), n_results, P.tiles, results, wg, s,
@@ -884,7 +884,7 @@ asmevo_status asmevo_diff_cosine_nd(const asmevo_segment_nd* segs, int32_t n, as
                                 reinterpret_cast<unsigned long long*>(ws + C.off_counters), cos_results,
                                 reinterpret_cast<const CosLevels*>(ws + C.off_lv),
                                 reinterpret_cast<const uint64_t*>(ws + C.off_prefix), C.groups,
-                                reinterpret_cast<double*>(ws + C.off_levels), short_rows));
+                                reinterpret_cast<double*>(ws + C.off_levels), variant));
   return ASMEVO_OK;
 }
 

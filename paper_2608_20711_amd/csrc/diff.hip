@@ -871,7 +871,10 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
   }
 }
 
-template <int DT, bool COS, bool ND>
+// ROWS: only segments of long rows, 16-byte aligned and unit-stride, of a
+// float type (the cosine variant for calls made only of such segments): the
+// row-tiled whole-tile code alone.
+template <int DT, bool COS, bool ND, bool ROWS = false>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                            uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
                                            double* partials, uint32_t& nonfinite, uint8_t* slot_bytes) {
@@ -969,7 +972,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     return;
   }
 
-  if constexpr (kCos) {
+  if constexpr (kCos && !ROWS) {
     if (S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks) {
       diff_range_narrow_cos<DT, ND>(S, X, t_begin, t_end, step, lane, acc, partials, nonfinite, tol_mode, strict,
                                     vec, gather, pair2a, pair2b, in_sa, in_sb, ibase0, permuted);
@@ -1008,7 +1011,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     // row here, with bounded loads: the bytes past the row's end load as zeros
     // on both sides, and adding a +0.0 product leaves a lane sum unchanged (a
     // lane sum starts at +0.0, so it is never -0.0).
-    if (whole || (kCos && vec && !gather)) {
+    if (ROWS || whole || (kCos && vec && !gather)) {
       // Whole tile: issue all loads first, then one combined check.
       u32x4 va[U], vb[U];
       uint32_t nv[U];                      // valid elements per chunk
@@ -1673,13 +1676,19 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 }
 
 
-// The cosine pass over N-D segments whose rows are all short and of a float
-// type (at least two rows of at most kNarrowCosChunks chunks each), for calls
-// made only of such segments: the dealing and the segment search of
-// diff_kernel<true, true>, every range taken by the short-row path.  Without
-// the other paths it needs 125 VGPRs, four waves per SIMD instead of three
-// (256-byte half rows: 3.99 against 4.27 ms; four chunks a lane ran slower,
-// 4.70 ms spilling at three waves per SIMD and 4.44 ms at two).
+// The cosine pass over N-D segments for calls made only of one kind of
+// float segment, with the dealing and the segment search of
+// diff_kernel<true, true> and one path of its code:
+// * narrow_cos_kernel: short rows (at least two rows of at most
+//   kNarrowCosChunks chunks each), the short-row path.  Without the other
+//   paths it needs 122 VGPRs, four waves per SIMD instead of three (256-byte
+//   half rows: 3.95-3.99 against 4.27 ms; four chunks a lane ran slower,
+//   4.70 ms spilling at three waves per SIMD and 4.44 ms at two).
+// * rows_cos_kernel: long rows, 16-byte aligned and unit-stride (one row, or
+//   rows of more than kNarrowCosChunks chunks), the row-tiled whole-tile code:
+//   140 VGPRs and no spill instead of 168 and six spilled (sliced rows 5.94
+//   against 6.19 ms, transposed and permuted views and a block table 2 %
+//   faster).
 template <int DT>
 __device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* X, uint64_t b, uint64_t e,
                                                  uint32_t step, uint32_t lane, Acc& acc, double* partials,
@@ -1692,10 +1701,11 @@ __device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* 
                                      permuted ? 0 : S.nd_index_base, permuted);
 }
 
-__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(4)))
-void narrow_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
-                       uint64_t total_tiles, asmevo_segment_result* results, double* partials,
-                       unsigned long long* nonfinite_pairs) {
+template <bool LONG_ROWS>
+__device__ __forceinline__ void split_cos_ranges(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext,
+                                                 int n, uint64_t total_tiles, asmevo_segment_result* results,
+                                                 double* partials, unsigned long long* nonfinite_pairs,
+                                                 uint8_t* slot) {
   constexpr uint32_t kStep = ASMEVO_COS_WAVE_STEP;
   constexpr uint64_t kDeal = ASMEVO_COS_DEAL;
   static_assert(kDeal > 0 && (kDiffBlock / kWave) % kStep == 0, "blocks dealt inside a workgroup");
@@ -1745,20 +1755,53 @@ void narrow_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict
       const uint64_t t_end = seg_end < hi ? seg_end : hi;
       const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
       const NdExt* X = S.nd_ext != ~0ull ? ext + S.nd_ext : nullptr;
-      switch (S.dtype) {
-        case ASMEVO_F32: narrow_cos_range<ASMEVO_F32>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_BF16: narrow_cos_range<ASMEVO_BF16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_F16: narrow_cos_range<ASMEVO_F16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
-        case ASMEVO_FP8_E4M3:
-          narrow_cos_range<ASMEVO_FP8_E4M3>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
-          break;
-        default: break;                  // not launched for other types
+      if constexpr (LONG_ROWS) {
+        switch (S.dtype) {
+          case ASMEVO_F32:
+            diff_range<ASMEVO_F32, true, true, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_BF16:
+            diff_range<ASMEVO_BF16, true, true, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_F16:
+            diff_range<ASMEVO_F16, true, true, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_FP8_E4M3:
+            diff_range<ASMEVO_FP8_E4M3, true, true, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          default: break;                // not launched for other types
+        }
+      } else {
+        switch (S.dtype) {
+          case ASMEVO_F32: narrow_cos_range<ASMEVO_F32>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+          case ASMEVO_BF16: narrow_cos_range<ASMEVO_BF16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+          case ASMEVO_F16: narrow_cos_range<ASMEVO_F16>(S, X, b, e, kStep, lane, acc, partials, nonfinite); break;
+          case ASMEVO_FP8_E4M3:
+            narrow_cos_range<ASMEVO_FP8_E4M3>(S, X, b, e, kStep, lane, acc, partials, nonfinite);
+            break;
+          default: break;                // not launched for other types
+        }
       }
       flush<false>(acc, S, results, lane, nonfinite, nonfinite_pairs);
       t += (t_end - t + kStep - 1) / kStep * kStep;   // this wave's first tile at or after t_end
     }
   }
 }
+__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(4)))
+void narrow_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
+                       uint64_t total_tiles, asmevo_segment_result* results, double* partials,
+                       unsigned long long* nonfinite_pairs) {
+  split_cos_ranges<false>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, nullptr);
+}
+
+__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(ASMEVO_COS_WAVES_PER_EU)))
+void rows_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
+                     uint64_t total_tiles, asmevo_segment_result* results, double* partials,
+                     unsigned long long* nonfinite_pairs) {
+  __shared__ __align__(16) uint8_t slot[16];     // unused by the cosine variant's code
+  split_cos_ranges<true>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, slot);
+}
+
 }  // namespace
 
 // Resident workgroups per CU of a diff kernel (one code object: queried once).
@@ -1780,27 +1823,37 @@ int diff_nd_blocks_per_cu() { return resident_blocks<false, true>(); }
 
 int cos_nd_blocks_per_cu() { return resident_blocks<true, true>(); }
 
-int narrow_cos_blocks_per_cu() {
-  static const int blocks = [] {
+int split_cos_blocks_per_cu(int variant) {
+  static const int narrow = [] {
     int b = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, narrow_cos_kernel, kDiffBlock, 0) != hipSuccess || b <= 0)
       b = 3;
     return b;
   }();
-  return blocks;
+  static const int rows = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, rows_cos_kernel, kDiffBlock, 0) != hipSuccess || b <= 0)
+      b = 3;
+    return b;
+  }();
+  return variant == kCosNdShortRows ? narrow : rows;
 }
 
-bool cos_nd_short_rows_only(const DiffSeg* segs, int n) {
-  bool any = false;
+int cos_nd_variant(const DiffSeg* segs, int n) {
+  bool any = false, all_short = true, all_long = true;
   for (int k = 0; k < n; ++k) {
     const DiffSeg& S = segs[k];
     if (S.tile_count == 0) continue;
     const bool fp = S.dtype == ASMEVO_F32 || S.dtype == ASMEVO_BF16 || S.dtype == ASMEVO_F16 ||
                     S.dtype == ASMEVO_FP8_E4M3;
-    if (!fp || S.rows < 2 || S.row_chunks > (uint64_t)kNarrowCosChunks) return false;
+    if (!fp) return kCosNdMixed;
+    const bool short_rows = S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks;
+    all_short = all_short && short_rows;
+    all_long = all_long && !short_rows && (S.flags & kSegVec) != 0 && (S.flags & kSegGather) == 0;
     any = true;
   }
-  return any;
+  if (!any) return kCosNdMixed;
+  return all_short ? kCosNdShortRows : all_long ? kCosNdLongRows : kCosNdMixed;
 }
 
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
@@ -1865,7 +1918,7 @@ hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, c
                                  int workgroups, hipStream_t stream, double* partials,
                                  unsigned long long* nonfinite_pairs, asmevo_cosine_result* cos_results,
                                  const CosLevels* levels_of, const uint64_t* level_prefix,
-                                 const uint64_t* level_groups, double* levels, bool short_rows) {
+                                 const uint64_t* level_groups, double* levels, int variant) {
   if (n_results == 0) return hipSuccess;
   hipLaunchKernelGGL(diff_init_kernel, dim3((n_results + 255) / 256), dim3(256), 0, stream, results, n_results,
                      nonfinite_pairs);
@@ -1874,8 +1927,11 @@ hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, c
   if (n > 0 && total_tiles > 0) {
     const uint64_t max_wg = (total_tiles + (kDiffBlock / kWave) - 1) / (kDiffBlock / kWave);
     const int wg = (uint64_t)workgroups > max_wg ? (int)max_wg : workgroups;
-    if (short_rows)
+    if (variant == kCosNdShortRows)
       hipLaunchKernelGGL(narrow_cos_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n, total_tiles,
+                         results, partials, nonfinite_pairs);
+    else if (variant == kCosNdLongRows)
+      hipLaunchKernelGGL(rows_cos_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n, total_tiles,
                          results, partials, nonfinite_pairs);
     else
       hipLaunchKernelGGL((diff_kernel<true, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,

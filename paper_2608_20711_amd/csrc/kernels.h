@@ -38,24 +38,26 @@ hipError_t launch_diff_nd(const DiffSeg* segs, const NdExt* ext, int n, int n_re
                           uint64_t total_tiles, asmevo_segment_result* results, int workgroups,
                           hipStream_t stream);
 
-// Resident workgroups per CU of the N-D cosine pass, and of its variant for
-// calls whose segments all have short rows of a float type.
+// The N-D cosine pass's kernel for a call: the general one, or a variant for
+// calls whose segments (those with tiles) are all of a float type and all
+// short rows, or all long 16-byte-aligned unit-stride rows.
+enum { kCosNdMixed = 0, kCosNdShortRows = 1, kCosNdLongRows = 2 };
+// The variant for these descriptors (host copies of the device descriptors).
+int cos_nd_variant(const DiffSeg* segs, int n);
+// Resident workgroups per CU of the general N-D cosine kernel, and of a variant.
 int cos_nd_blocks_per_cu();
-int narrow_cos_blocks_per_cu();
-// Whether every segment with tiles (host copies of the device descriptors)
-// has short rows of a float type, so the N-D cosine pass may take the variant.
-bool cos_nd_short_rows_only(const DiffSeg* segs, int n);
+int split_cos_blocks_per_cu(int variant);
 // Diff and cosine term of N-D segments: the diff as launch_diff_nd, the block
 // sums per tile as launch_diff; the block trees run over `units`, one
 // descriptor per result (its first tile, its tile count, dtype, element
 // count), so the tables (levels_of, level_prefix, counters) are per result.
-// short_rows: launch the short-row variant (cos_nd_short_rows_only).
+// variant: the kernel to launch (cos_nd_variant).
 hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, const DiffSeg* units,
                                  int n_results, uint64_t total_tiles, asmevo_segment_result* results,
                                  int workgroups, hipStream_t stream, double* partials,
                                  unsigned long long* nonfinite_pairs, asmevo_cosine_result* cos_results,
                                  const CosLevels* levels_of, const uint64_t* level_prefix,
-                                 const uint64_t* level_groups, double* levels, bool short_rows);
+                                 const uint64_t* level_groups, double* levels, int variant);
 
 hipError_t launch_copy(const CopyRegion* regs, int n, uint64_t total_tiles, int workgroups,
                        hipStream_t stream);

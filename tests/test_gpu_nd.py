@@ -401,10 +401,11 @@ def test_cosine_row_tails_nd(dtype):
     """Rows of more than 32 chunks whose last tile is partial, tiled row by
     row: rows 16-byte aligned (every chunk of the last tile loaded, the
     lanes past the row's whole chunks cleared, a partial last chunk read
-    element by element), rows off 16 bytes (chunk by chunk), lengths that
-    end on a chunk boundary or inside a chunk, and single rows shorter than
-    one chunk; against the oracle's exact sums within the order's bound and
-    bit for bit against the order model."""
+    element by element) with single rows shorter than one chunk, in a call
+    of their own (the kernel for long aligned rows), and rows off 16 bytes
+    (chunk by chunk) in another; lengths that end on a chunk boundary or
+    inside a chunk; against the oracle's exact sums within the order's bound
+    and bit for bit against the order model."""
     rng = np.random.default_rng(24)
     es = np.dtype(NP_T[dtype]).itemsize
     epc = 16 // es
@@ -412,16 +413,16 @@ def test_cosine_row_tails_nd(dtype):
     b = rng.standard_normal((3, 5, width)).astype(NP_T[dtype])
     a = _perturbed(b, rng, frac=0.002)
     lengths = [256 * epc + 3, 257 * epc + epc // 2, 175 * epc, 33 * epc + 1, 40 * epc - 1]
-    views = []
-    for n in lengths:
-        views.append(lambda x, n=n: x[:, :, epc:epc + n])         # aligned rows
-        views.append(lambda x, n=n: x[:, 1:4, 1:1 + n])            # rows off 16 bytes
-    views += [lambda x: x[1, 2, epc:epc + 3], lambda x: x[2, 0, 0:1], lambda x: x[0, 4, epc:2 * epc - 1]]
-    specs = [_spec(v(a), a, b, dtype, result=k, index_base=11 * k, view_b=v(b)) for k, v in enumerate(views)]
-    got, want, cgot, cwant = _run_cos(specs, a, b, len(specs))
-    assert_results_equal(got, want, f"{dtype} row tails diff")
-    assert_cosine(cgot, *cwant, f"{dtype} row tails cosine")
-    assert all(c["blocks"] > 0 for c in cgot)
+    aligned = [lambda x, n=n: x[:, :, epc:epc + n] for n in lengths]
+    aligned += [lambda x: x[1, 2, epc:epc + 3], lambda x: x[2, 0, 0:1], lambda x: x[0, 4, epc:2 * epc - 1]]
+    unaligned = [lambda x, n=n: x[:, 1:4, 1:1 + n] for n in lengths]
+    # one call of aligned rows only (the long-row kernel), one of rows off 16 bytes
+    for name, views in (("aligned", aligned), ("unaligned", unaligned)):
+        specs = [_spec(v(a), a, b, dtype, result=k, index_base=11 * k, view_b=v(b)) for k, v in enumerate(views)]
+        got, want, cgot, cwant = _run_cos(specs, a, b, len(specs))
+        assert_results_equal(got, want, f"{dtype} {name} row tails diff")
+        assert_cosine(cgot, *cwant, f"{dtype} {name} row tails cosine")
+        assert all(c["blocks"] > 0 for c in cgot)
 
 
 def test_cosine_block_table_at_scale_equals_gathered_copy():
