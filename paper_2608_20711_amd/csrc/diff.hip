@@ -873,8 +873,10 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
 
 // ROWS: only segments of long rows, 16-byte aligned and unit-stride, of a
 // float type (the cosine variant for calls made only of such segments): the
-// row-tiled whole-tile code alone.
-template <int DT, bool COS, bool ND, bool ROWS = false>
+// row-tiled whole-tile code alone.  GATHERS: only gathers of long rows (one
+// row, or rows of more than kNarrowCosChunks chunks) of a float type: the
+// chunk-by-chunk code alone, two chunks in flight.
+template <int DT, bool COS, bool ND, bool ROWS = false, bool GATHERS = false>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                            uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
                                            double* partials, uint32_t& nonfinite, uint8_t* slot_bytes) {
@@ -972,7 +974,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     return;
   }
 
-  if constexpr (kCos && !ROWS) {
+  if constexpr (kCos && !ROWS && !GATHERS) {
     if (S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks) {
       diff_range_narrow_cos<DT, ND>(S, X, t_begin, t_end, step, lane, acc, partials, nonfinite, tol_mode, strict,
                                     vec, gather, pair2a, pair2b, in_sa, in_sb, ibase0, permuted);
@@ -1011,7 +1013,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
     // row here, with bounded loads: the bytes past the row's end load as zeros
     // on both sides, and adding a +0.0 product leaves a lane sum unchanged (a
     // lane sum starts at +0.0, so it is never -0.0).
-    if (ROWS || whole || (kCos && vec && !gather)) {
+    if (!GATHERS && (ROWS || whole || (kCos && vec && !gather))) {
       // Whole tile: issue all loads first, then one combined check.
       u32x4 va[U], vb[U];
       uint32_t nv[U];                      // valid elements per chunk
@@ -1213,6 +1215,41 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
         nv[j] = nb[j] / es;
       }
       tile_slow<DT, ND, !COS, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X, permuted, slot);
+      continue;
+    }
+    if constexpr (GATHERS) {
+      // the same chunks in the same order, two in flight
+#pragma unroll 1
+      for (int j = 0; j < U; j += 2) {
+        u32x4 va[2], vb[2];
+        uint32_t nb[2];
+        uint64_t c[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          c[h] = k0 + (uint64_t)((j + h) * kWave) + lane;
+          va[h] = u32x4{0u, 0u, 0u, 0u};
+          vb[h] = u32x4{0u, 0u, 0u, 0u};
+          nb[h] = 0;
+          if (c[h] < S.row_chunks) {
+            const uint64_t rem = S.row_bytes - c[h] * kChunk;
+            nb[h] = rem < (uint64_t)kChunk ? (uint32_t)rem : (uint32_t)kChunk;
+            load_nd_chunk<DT>(pa, pb, c[h], nb[h], vec, gather, in_sa, in_sb, pair2a, pair2b,
+                              c[h] + 1 == S.row_chunks, va[h], vb[h]);
+          }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          chunk<DT, ND>(va[h], vb[h], ibase + c[h] * epc, nb[h] / es, tol_mode, strict, S.atol, S.rtol, acc, X,
+                        permuted);
+          const Cos keep = cs;
+          cos_chunk_fast<DT>(va[h], vb[h], cs);
+          if (!(__builtin_isfinite(cs.ab) && __builtin_isfinite(cs.aa) && __builtin_isfinite(cs.bb))) {
+            cs = keep;
+            cos_chunk<DT>(va[h], vb[h], nb[h] / es, cs, nonfinite);
+          }
+        }
+      }
+      cos_store(cs, partials + kCosRec * (S.tile_begin + tile), lane);
       continue;
     }
 #pragma unroll 1
@@ -1689,6 +1726,9 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 //   140 VGPRs and no spill instead of 168 and six spilled (sliced rows 5.94
 //   against 6.19 ms, transposed and permuted views and a block table 2 %
 //   faster).
+// * gather_cos_kernel: gathers of long rows, the chunk-by-chunk code with two
+//   chunks in flight: 107 VGPRs, four waves per SIMD (the stride-2 gather:
+//   5.68 against 6.05 ms).
 template <int DT>
 __device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* X, uint64_t b, uint64_t e,
                                                  uint32_t step, uint32_t lane, Acc& acc, double* partials,
@@ -1701,7 +1741,7 @@ __device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* 
                                      permuted ? 0 : S.nd_index_base, permuted);
 }
 
-template <bool LONG_ROWS>
+template <int KIND>   // kCosNdShortRows, kCosNdLongRows or kCosNdGathers
 __device__ __forceinline__ void split_cos_ranges(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext,
                                                  int n, uint64_t total_tiles, asmevo_segment_result* results,
                                                  double* partials, unsigned long long* nonfinite_pairs,
@@ -1755,7 +1795,24 @@ __device__ __forceinline__ void split_cos_ranges(const DiffSeg* __restrict__ seg
       const uint64_t t_end = seg_end < hi ? seg_end : hi;
       const uint64_t b = t - S.tile_begin, e = t_end - S.tile_begin;
       const NdExt* X = S.nd_ext != ~0ull ? ext + S.nd_ext : nullptr;
-      if constexpr (LONG_ROWS) {
+      if constexpr (KIND == kCosNdGathers) {
+        switch (S.dtype) {
+          case ASMEVO_F32:
+            diff_range<ASMEVO_F32, true, true, false, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_BF16:
+            diff_range<ASMEVO_BF16, true, true, false, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_F16:
+            diff_range<ASMEVO_F16, true, true, false, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
+            break;
+          case ASMEVO_FP8_E4M3:
+            diff_range<ASMEVO_FP8_E4M3, true, true, false, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite,
+                                                                 slot);
+            break;
+          default: break;                // not launched for other types
+        }
+      } else if constexpr (KIND == kCosNdLongRows) {
         switch (S.dtype) {
           case ASMEVO_F32:
             diff_range<ASMEVO_F32, true, true, true>(S, X, b, e, kStep, lane, acc, partials, nonfinite, slot);
@@ -1791,7 +1848,7 @@ __global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(4)))
 void narrow_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
                        uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                        unsigned long long* nonfinite_pairs) {
-  split_cos_ranges<false>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, nullptr);
+  split_cos_ranges<kCosNdShortRows>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, nullptr);
 }
 
 __global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(ASMEVO_COS_WAVES_PER_EU)))
@@ -1799,7 +1856,15 @@ void rows_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__
                      uint64_t total_tiles, asmevo_segment_result* results, double* partials,
                      unsigned long long* nonfinite_pairs) {
   __shared__ __align__(16) uint8_t slot[16];     // unused by the cosine variant's code
-  split_cos_ranges<true>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, slot);
+  split_cos_ranges<kCosNdLongRows>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, slot);
+}
+
+__global__ __launch_bounds__(kDiffBlock) __attribute__((amdgpu_waves_per_eu(ASMEVO_COS_WAVES_PER_EU)))
+void gather_cos_kernel(const DiffSeg* __restrict__ segs, const NdExt* __restrict__ ext, int n,
+                       uint64_t total_tiles, asmevo_segment_result* results, double* partials,
+                       unsigned long long* nonfinite_pairs) {
+  __shared__ __align__(16) uint8_t slot[16];     // unused by the cosine variant's code
+  split_cos_ranges<kCosNdGathers>(segs, ext, n, total_tiles, results, partials, nonfinite_pairs, slot);
 }
 
 }  // namespace
@@ -1836,11 +1901,17 @@ int split_cos_blocks_per_cu(int variant) {
       b = 3;
     return b;
   }();
-  return variant == kCosNdShortRows ? narrow : rows;
+  static const int gathers = [] {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, gather_cos_kernel, kDiffBlock, 0) != hipSuccess || b <= 0)
+      b = 3;
+    return b;
+  }();
+  return variant == kCosNdShortRows ? narrow : variant == kCosNdLongRows ? rows : gathers;
 }
 
 int cos_nd_variant(const DiffSeg* segs, int n) {
-  bool any = false, all_short = true, all_long = true;
+  bool any = false, all_short = true, all_long = true, all_gathers = true;
   for (int k = 0; k < n; ++k) {
     const DiffSeg& S = segs[k];
     if (S.tile_count == 0) continue;
@@ -1850,10 +1921,11 @@ int cos_nd_variant(const DiffSeg* segs, int n) {
     const bool short_rows = S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks;
     all_short = all_short && short_rows;
     all_long = all_long && !short_rows && (S.flags & kSegVec) != 0 && (S.flags & kSegGather) == 0;
+    all_gathers = all_gathers && !short_rows && (S.flags & kSegGather) != 0;
     any = true;
   }
   if (!any) return kCosNdMixed;
-  return all_short ? kCosNdShortRows : all_long ? kCosNdLongRows : kCosNdMixed;
+  return all_short ? kCosNdShortRows : all_long ? kCosNdLongRows : all_gathers ? kCosNdGathers : kCosNdMixed;
 }
 
 hipError_t launch_diff(const DiffSeg* segs, int n, uint64_t total_tiles,
@@ -1932,6 +2004,9 @@ hipError_t launch_diff_cosine_nd(const DiffSeg* segs, const NdExt* ext, int n, c
                          results, partials, nonfinite_pairs);
     else if (variant == kCosNdLongRows)
       hipLaunchKernelGGL(rows_cos_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n, total_tiles,
+                         results, partials, nonfinite_pairs);
+    else if (variant == kCosNdGathers)
+      hipLaunchKernelGGL(gather_cos_kernel, dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n, total_tiles,
                          results, partials, nonfinite_pairs);
     else
       hipLaunchKernelGGL((diff_kernel<true, true>), dim3(wg), dim3(kDiffBlock), 0, stream, segs, ext, n,
