@@ -874,8 +874,9 @@ __device__ __forceinline__ void diff_range_narrow_cos(const DiffSeg& S, const Nd
 // ROWS: only segments of long rows, 16-byte aligned and unit-stride, of a
 // float type (the cosine variant for calls made only of such segments): the
 // row-tiled whole-tile code alone.  GATHERS: only gathers of long rows (one
-// row, or rows of more than kNarrowCosChunks chunks) of a float type: the
-// chunk-by-chunk code alone, two chunks in flight.
+// row, or rows of more than kNarrowCosChunks chunks) of a float type whose
+// elements are 2 apart in both operands: the chunk-by-chunk code alone, two
+// chunks in flight, each a pair of 16-byte loads per operand.
 template <int DT, bool COS, bool ND, bool ROWS = false, bool GATHERS = false>
 __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uint64_t t_begin,
                                            uint64_t t_end, uint32_t step, uint32_t lane, Acc& acc,
@@ -1217,7 +1218,7 @@ __device__ __forceinline__ void diff_range(const DiffSeg& S, const NdExt* X, uin
       tile_slow<DT, ND, !COS, U>(va, vb, i0, nv, lane, tol_mode, strict, S.atol, S.rtol, acc, X, permuted, slot);
       continue;
     }
-    if constexpr (GATHERS) {
+    if (GATHERS && pair2a && pair2b) {
       // the same chunks in the same order, two in flight
 #pragma unroll 1
       for (int j = 0; j < U; j += 2) {
@@ -1726,9 +1727,12 @@ __global__ __launch_bounds__(kCosBlock) void cosine_kernel(const DiffSeg* __rest
 //   140 VGPRs and no spill instead of 168 and six spilled (sliced rows 5.94
 //   against 6.19 ms, transposed and permuted views and a block table 2 %
 //   faster).
-// * gather_cos_kernel: gathers of long rows, the chunk-by-chunk code with two
-//   chunks in flight: 107 VGPRs, four waves per SIMD (the stride-2 gather:
-//   5.68 against 6.05 ms).
+// * gather_cos_kernel: gathers of long rows with elements 2 apart in both
+//   operands, the chunk-by-chunk code with two chunks in flight: four waves
+//   per SIMD (the stride-2 gather: 5.68 against 6.07 ms).  Gathers whose
+//   elements load one by one stay in diff_kernel<true, true>: in this kernel
+//   the stride-3 gather ran 6.29 ms with two chunks in flight (1.8 % more
+//   fetched) and 6.56 ms with one, against 5.89.
 template <int DT>
 __device__ __forceinline__ void narrow_cos_range(const DiffSeg& S, const NdExt* X, uint64_t b, uint64_t e,
                                                  uint32_t step, uint32_t lane, Acc& acc, double* partials,
@@ -1921,7 +1925,8 @@ int cos_nd_variant(const DiffSeg* segs, int n) {
     const bool short_rows = S.rows > 1 && S.row_chunks <= (uint64_t)kNarrowCosChunks;
     all_short = all_short && short_rows;
     all_long = all_long && !short_rows && (S.flags & kSegVec) != 0 && (S.flags & kSegGather) == 0;
-    all_gathers = all_gathers && !short_rows && (S.flags & kSegGather) != 0;
+    all_gathers = all_gathers && !short_rows && (S.flags & kSegGather) != 0 && (S.flags & kSegPair2A) != 0 &&
+                  (S.flags & kSegPair2B) != 0;
     any = true;
   }
   if (!any) return kCosNdMixed;

@@ -41,7 +41,7 @@ hipError_t launch_diff_nd(const DiffSeg* segs, const NdExt* ext, int n, int n_re
 // The N-D cosine pass's kernel for a call: the general one, or a variant for
 // calls whose segments (those with tiles) are all of a float type and all
 // short rows, all long 16-byte-aligned unit-stride rows, or all gathers of
-// long rows.
+// long rows with elements 2 apart in both operands.
 enum { kCosNdMixed = 0, kCosNdShortRows = 1, kCosNdLongRows = 2, kCosNdGathers = 3 };
 // The variant for these descriptors (host copies of the device descriptors).
 int cos_nd_variant(const DiffSeg* segs, int n);

@@ -403,8 +403,9 @@ def test_cosine_row_tails_nd(dtype):
     lanes past the row's whole chunks cleared, a partial last chunk read
     element by element) with single rows shorter than one chunk, in a call
     of their own (the kernel for long aligned rows), rows off 16 bytes
-    (chunk by chunk) in another, and long gathers (strides 2, 3 and 5, rows
-    16-byte aligned or not, a partial last chunk) in a third (the gathers'
+    (chunk by chunk) in another, long gathers (strides 2, 3 and 5, rows
+    16-byte aligned or not, a partial last chunk) in a third, and gathers of
+    elements 2 apart in 16-byte-aligned rows in a fourth (the gathers'
     kernel); lengths that end on a chunk boundary or inside a chunk; against
     the oracle's exact sums within the order's bound and bit for bit against
     the order model."""
@@ -419,9 +420,12 @@ def test_cosine_row_tails_nd(dtype):
     aligned += [lambda x: x[1, 2, epc:epc + 3], lambda x: x[2, 0, 0:1], lambda x: x[0, 4, epc:2 * epc - 1]]
     unaligned = [lambda x, n=n: x[:, 1:4, 1:1 + n] for n in lengths]
     gathers = [lambda x: x[:, :, ::2], lambda x: x[:, :, 1::3], lambda x: x[:, 1:4, 3::2], lambda x: x[0, 0, ::5]]
+    pairs = [lambda x: x[:, :, ::2], lambda x: x[:, 2:5, 2 * epc::2], lambda x: x[1, 1, ::2],
+             lambda x: x[:, 2:5, 2 * epc:2 * epc + 2 * 521:2]]      # the last chunk partial
     # one call of aligned rows only (the long-row kernel), one of rows off 16
-    # bytes, one of gathers only (the gathers' kernel)
-    for name, views in (("aligned", aligned), ("unaligned", unaligned), ("gathers", gathers)):
+    # bytes, one of gathers, one of gathers of elements 2 apart whose rows are
+    # 16-byte aligned (the gathers' kernel)
+    for name, views in (("aligned", aligned), ("unaligned", unaligned), ("gathers", gathers), ("pairs", pairs)):
         specs = [_spec(v(a), a, b, dtype, result=k, index_base=11 * k, view_b=v(b)) for k, v in enumerate(views)]
         got, want, cgot, cwant = _run_cos(specs, a, b, len(specs))
         assert_results_equal(got, want, f"{dtype} {name} row tails diff")
